@@ -1,0 +1,368 @@
+"""CPU oracle for the Mira per-layer MoE expert step (test infrastructure).
+
+This module is the plain, slow, fp64 statement of what the GPU library
+computes.  It is test infrastructure only: the tests, the smoke check and the
+CPU-baseline leg of the benchmark import it; the product path never does, and
+it shares no code, constants or helpers with the HIP library.
+
+Paper: "Memory-Efficient MoE Inference Using Adaptive Caching and Predictive
+Expert Staging" (Mira).  Each function names the passage it follows.
+
+Readings of passages the paper leaves open (each is also listed in the design
+notes of the repository):
+
+* Packing (section IV-B, the alpha_r / s_r displays and Eqs. (2)-(4)): the
+  scale is computed in fp32 as fl32(max(alpha_r, eps) / 127), rounded to the
+  stored BF16 value sigma_r (round to nearest, ties to even), and the integers
+  are computed against that stored sigma_r, so the stored scale is exactly the
+  one the integers were made with.  round() is round-half-to-even applied to
+  the correctly rounded fp32 quotient w / sigma_r; the clamp to [-127, 127]
+  follows the rounding.
+* Packed byte layout (section IV-B and the memory-layout figure only say the
+  three INT8 matrices and the shared scale travel together): one blob per
+  expert, little-endian, int8 gate [R][C], int8 up [R][C], int8 down [C][R],
+  bf16 sigma [R], zero padding up to a multiple of 256 bytes.
+* Matrix roles: the paper calls W1 the up projection and W3 the gate
+  modulation without writing the FFN formula.  The library names matrices by
+  role: "gate" goes through SiLU, "up" is the linear branch (Mixtral's w1 and
+  w3 respectively); the shared scale treats both alike.
+* Router and combine (section II-A): logits = x . Wg^T + b, top-k by value
+  descending with the lower expert index winning ties; combine weights are a
+  softmax over the k selected logits (renormalised top-k); shared experts, if
+  any, are added with weight 1.
+* Permutation: (token, slot) pairs p = t*k + j are grouped by expert with a
+  stable counting sort; shared-expert pairs follow the routed ones, in token
+  order.
+* Predictor (section IV-E, with the MLP shape of the workload): mean-pool a
+  group of token rows, z = ReLU(W1 f + b1), scores = sigmoid(W2 z + b2).
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+__all__ = [
+    "BLOB_ALIGN",
+    "bf16_bits_from_f32",
+    "f32_from_bf16_bits",
+    "packed_expert_bytes",
+    "pack_expert",
+    "unpack_expert",
+    "dequantize_expert",
+    "router_logits",
+    "topk_select",
+    "near_tie_tokens",
+    "combine_weights",
+    "permute_pairs",
+    "expert_ffn",
+    "moe_forward",
+    "predictor_scores",
+    "coverage_at_k",
+]
+
+BLOB_ALIGN = 256  # packed blobs are zero-padded to a multiple of this many bytes
+
+
+# ----------------------------------------------------------------------------
+# bf16 helpers (the storage type of the shared scale, section IV-B)
+# ----------------------------------------------------------------------------
+
+def bf16_bits_from_f32(v):
+    """Round fp32 values to the nearest bf16 value, ties to even.
+
+    Written from the definition: bf16 keeps the top 16 bits of the fp32
+    pattern.  Of the two bf16 neighbours of v (truncate, and truncate plus one
+    unit in the last place) take the nearer; on an exact tie take the one
+    whose last kept bit is zero.  Inputs must be finite.
+    """
+    a = np.ascontiguousarray(np.asarray(v, dtype=np.float32))
+    if not np.all(np.isfinite(a)):
+        raise ValueError("bf16 rounding of a non-finite value is out of contract")
+    bits = a.view(np.uint32).astype(np.uint64)
+    lo = bits >> 16                       # truncated pattern (toward zero)
+    rem = bits & 0xFFFF                   # dropped half-word
+    up = (rem > 0x8000) | ((rem == 0x8000) & ((lo & 1) == 1))
+    out = lo + up.astype(np.uint64)
+    return out.astype(np.uint16)
+
+
+def f32_from_bf16_bits(b):
+    """Exact widening of bf16 bit patterns to fp32."""
+    b = np.asarray(b, dtype=np.uint16).astype(np.uint32) << 16
+    return b.view(np.float32)
+
+
+# ----------------------------------------------------------------------------
+# a0: packing (section IV-B, alpha_r and s_r displays, Eqs. (2)-(4))
+# ----------------------------------------------------------------------------
+
+def packed_expert_bytes(C: int, R: int) -> int:
+    """Bytes of one packed expert: 3*R*C int8 plus R bf16 scales, padded to 256."""
+    raw = 3 * R * C + 2 * R
+    return (raw + BLOB_ALIGN - 1) // BLOB_ALIGN * BLOB_ALIGN
+
+
+def _shared_row_scale(w_gate, w_up, w_down, eps):
+    """alpha_r, then s_r = max(alpha_r, eps) / 127 in fp32, then bf16 storage."""
+    alpha = np.maximum(
+        np.maximum(np.abs(w_gate).max(axis=1), np.abs(w_up).max(axis=1)),
+        np.abs(w_down).max(axis=0),
+    ).astype(np.float32)
+    s32 = (np.maximum(alpha, np.float32(eps)) / np.float32(127.0)).astype(np.float32)
+    sigma_bits = bf16_bits_from_f32(s32)
+    return alpha, s32, sigma_bits
+
+
+def _quantize(w, sigma):
+    """q = clamp(round(w / sigma), -127, 127), with fp32 division and ties to even."""
+    quot = (w / sigma).astype(np.float32)           # correctly rounded fp32 quotient
+    q = np.rint(quot)                               # round half to even
+    q = np.clip(q, -127.0, 127.0)
+    return q.astype(np.int8)
+
+
+def pack_expert(w_gate, w_up, w_down, eps=1e-8):
+    """Pack one expert into the canonical blob (uint8 array).
+
+    w_gate, w_up: [R][C]; w_down: [C][R]; fp32 (bf16 inputs upcast exactly).
+    Returns the blob of packed_expert_bytes(C, R) bytes.
+    """
+    w_gate = np.asarray(w_gate, dtype=np.float32)
+    w_up = np.asarray(w_up, dtype=np.float32)
+    w_down = np.asarray(w_down, dtype=np.float32)
+    R, C = w_gate.shape
+    if w_up.shape != (R, C) or w_down.shape != (C, R):
+        raise ValueError("expected gate/up [R][C] and down [C][R]")
+    if not (np.all(np.isfinite(w_gate)) and np.all(np.isfinite(w_up)) and np.all(np.isfinite(w_down))):
+        raise ValueError("non-finite weights are out of contract")
+    _, _, sigma_bits = _shared_row_scale(w_gate, w_up, w_down, eps)
+    sigma = f32_from_bf16_bits(sigma_bits)
+    q_gate = _quantize(w_gate, sigma[:, None])
+    q_up = _quantize(w_up, sigma[:, None])
+    q_down = _quantize(w_down, sigma[None, :])
+
+    blob = np.zeros(packed_expert_bytes(C, R), dtype=np.uint8)
+    o = 0
+    for part in (q_gate, q_up, q_down):
+        n = part.size
+        blob[o:o + n] = part.reshape(-1).view(np.uint8)
+        o += n
+    blob[o:o + 2 * R] = sigma_bits.astype("<u2").view(np.uint8)
+    return blob
+
+
+def unpack_expert(blob, C: int, R: int):
+    """Inverse of the byte layout: (q_gate [R][C], q_up [R][C], q_down [C][R], sigma_bits [R])."""
+    blob = np.asarray(blob, dtype=np.uint8)
+    if blob.size < 3 * R * C + 2 * R:
+        raise ValueError("blob too small for the given shape")
+    rc = R * C
+    q_gate = blob[0:rc].view(np.int8).reshape(R, C)
+    q_up = blob[rc:2 * rc].view(np.int8).reshape(R, C)
+    q_down = blob[2 * rc:3 * rc].view(np.int8).reshape(C, R)
+    sigma_bits = blob[3 * rc:3 * rc + 2 * R].view("<u2").astype(np.uint16)
+    return q_gate, q_up, q_down, sigma_bits
+
+
+def dequantize_expert(blob, C: int, R: int):
+    """c2: W_hat = sigma_r * q (fp64, exact) for the three matrices."""
+    q_gate, q_up, q_down, sigma_bits = unpack_expert(blob, C, R)
+    sigma = f32_from_bf16_bits(sigma_bits).astype(np.float64)
+    wg = q_gate.astype(np.float64) * sigma[:, None]
+    wu = q_up.astype(np.float64) * sigma[:, None]
+    wd = q_down.astype(np.float64) * sigma[None, :]
+    return wg, wu, wd
+
+
+# ----------------------------------------------------------------------------
+# a1-a3: router, top-k, combine weights, permutation (section II-A)
+# ----------------------------------------------------------------------------
+
+def router_logits(x, w_router, bias=None):
+    """Router scores over experts: l[t, e] = sum_c x[t, c] * Wg[e, c] + b[e], fp64."""
+    x = np.asarray(x, dtype=np.float64)
+    wg = np.asarray(w_router, dtype=np.float64)
+    logits = x @ wg.T
+    if bias is not None:
+        logits = logits + np.asarray(bias, dtype=np.float64)[None, :]
+    return logits
+
+
+def topk_select(logits, k: int):
+    """Top-k experts per token: value descending, lower index first on ties."""
+    logits = np.asarray(logits, dtype=np.float64)
+    if not np.all(np.isfinite(logits)):
+        raise ValueError("non-finite router logits are out of contract")
+    T, E = logits.shape
+    if not 1 <= k <= E:
+        raise ValueError("need 1 <= k <= E")
+    idx = np.empty((T, k), dtype=np.int32)
+    for t in range(T):
+        # lexsort sorts by the last key first: primary -logit, secondary index
+        order = np.lexsort((np.arange(E), -logits[t]))
+        idx[t] = order[:k]
+    return idx
+
+
+def near_tie_tokens(logits, k: int, delta: float = 1e-4):
+    """Tokens whose top-(k+1) sorted logits have an adjacent gap below delta.
+
+    On such tokens a different but equally valid rounding of the logits can
+    change the selected set or its order, so callers treat them as ambiguous.
+    """
+    logits = np.asarray(logits, dtype=np.float64)
+    T, E = logits.shape
+    m = min(k + 1, E)
+    out = []
+    for t in range(T):
+        s = np.sort(logits[t])[::-1][:m]
+        if m > 1 and np.min(s[:-1] - s[1:]) < delta:
+            out.append(t)
+    return np.asarray(out, dtype=np.int64)
+
+
+def combine_weights(logits, idx, norm_topk: bool = True):
+    """Weights of the selected experts.
+
+    norm_topk: softmax over the k selected logits (renormalised top-k).
+    Otherwise: softmax over all E logits, then the selected probabilities.
+    """
+    logits = np.asarray(logits, dtype=np.float64)
+    idx = np.asarray(idx)
+    T, k = idx.shape
+    w = np.empty((T, k), dtype=np.float64)
+    for t in range(T):
+        sel = logits[t, idx[t]]
+        if norm_topk:
+            e = np.exp(sel - sel.max())
+            w[t] = e / e.sum()
+        else:
+            full = np.exp(logits[t] - logits[t].max())
+            w[t] = full[idx[t]] / full.sum()
+    return w
+
+
+def permute_pairs(idx, n_experts: int, n_shared: int = 0):
+    """Stable grouping of the (token, slot) pairs by expert.
+
+    Routed pair p = t*k + j belongs to expert idx[t, j]; shared expert s owns
+    the pairs T*k + s*T + t, one per token.  Groups are ordered routed experts
+    0..E-1, then shared experts 0..S-1; inside a group pairs keep increasing
+    pair index.  Returns counts [E+S], offsets [E+S+1], perm, inv where perm[pos]
+    is the pair at position pos and inv[pair] its position.
+    """
+    idx = np.asarray(idx, dtype=np.int64)
+    T, k = idx.shape
+    G = n_experts + n_shared
+    P = T * k + n_shared * T
+    group = np.empty(P, dtype=np.int64)
+    group[:T * k] = idx.reshape(-1)
+    for s in range(n_shared):
+        group[T * k + s * T:T * k + (s + 1) * T] = n_experts + s
+    if T * k and (group[:T * k].min() < 0 or group[:T * k].max() >= n_experts):
+        raise ValueError("expert index out of range")
+    counts = np.zeros(G, dtype=np.int64)
+    for g in group:
+        counts[g] += 1
+    offsets = np.zeros(G + 1, dtype=np.int64)
+    offsets[1:] = np.cumsum(counts)
+    fill = offsets[:-1].copy()
+    perm = np.empty(P, dtype=np.int64)
+    for p in range(P):                          # visiting pairs in order keeps it stable
+        g = group[p]
+        perm[fill[g]] = p
+        fill[g] += 1
+    inv = np.empty(P, dtype=np.int64)
+    inv[perm] = np.arange(P)
+    return counts, offsets, perm, inv
+
+
+# ----------------------------------------------------------------------------
+# a5-a7: expert FFN and combine (sections IV-A, IV-F; fused dequant + FFN)
+# ----------------------------------------------------------------------------
+
+def _silu(g):
+    return g / (1.0 + np.exp(-g))
+
+
+def expert_ffn(blob, x_rows, C: int, R: int):
+    """SwiGLU expert on dequantized weights: y = Wd (silu(Wg x) * (Wu x)), fp64."""
+    wg, wu, wd = dequantize_expert(blob, C, R)
+    x = np.asarray(x_rows, dtype=np.float64).reshape(-1, C)
+    g = x @ wg.T
+    u = x @ wu.T
+    h = _silu(g) * u
+    return h @ wd.T
+
+
+def moe_forward(x, w_router, bias, blobs, k: int, C: int, R: int,
+                shared_blobs=(), norm_topk: bool = True, idx=None, tokens=None):
+    """One MoE layer (section II-A) over experts in the packed format.
+
+    blobs[e] is routed expert e's blob, shared_blobs[s] shared expert s's.
+    idx, if given, replaces the oracle's own top-k (used to evaluate an
+    alternative, equally valid selection on near-tie tokens).  tokens, if
+    given, restricts the computation to those token rows (outputs in that
+    order).  Returns out [T'][C] fp64 plus the routing intermediates.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    logits = router_logits(x, w_router, bias)
+    if idx is None:
+        idx = topk_select(logits, k)
+    idx = np.asarray(idx, dtype=np.int32)
+    w = combine_weights(logits, idx, norm_topk)
+    rows = np.arange(x.shape[0]) if tokens is None else np.asarray(tokens)
+    out = np.zeros((len(rows), C), dtype=np.float64)
+    E = len(blobs)
+    for e in range(E):                           # one expert at a time
+        sel_t, sel_j = [], []
+        for i, t in enumerate(rows):
+            for j in range(k):
+                if idx[t, j] == e:
+                    sel_t.append(i)
+                    sel_j.append(j)
+        if not sel_t:
+            continue
+        xs = x[rows[sel_t]]
+        y = expert_ffn(blobs[e], xs, C, R)
+        for n, (i, j) in enumerate(zip(sel_t, sel_j)):
+            out[i] += w[rows[i], j] * y[n]
+    for sb in shared_blobs:
+        out += expert_ffn(sb, x[rows], C, R)
+    return {"out": out, "logits": logits, "idx": idx, "w": w}
+
+
+# ----------------------------------------------------------------------------
+# a8: predictor head (section IV-E; MLP shape of the workload)
+# ----------------------------------------------------------------------------
+
+def predictor_scores(x, group: int, w1, b1, w2, b2):
+    """Scores over the experts of layer l+2 for each group of token rows.
+
+    f = mean of the group's rows of x; z = ReLU(W1 f + b1);
+    scores = 1 / (1 + exp(-(W2 z + b2))).  fp64.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    T, C = x.shape
+    if group <= 0 or T % group:
+        raise ValueError("T must be a positive multiple of group")
+    n = T // group
+    w1 = np.asarray(w1, dtype=np.float64)
+    w2 = np.asarray(w2, dtype=np.float64)
+    b1 = np.zeros(w1.shape[0]) if b1 is None else np.asarray(b1, dtype=np.float64)
+    b2 = np.zeros(w2.shape[0]) if b2 is None else np.asarray(b2, dtype=np.float64)
+    scores = np.empty((n, w2.shape[0]), dtype=np.float64)
+    for i in range(n):
+        f = x[i * group:(i + 1) * group].mean(axis=0)
+        z = np.maximum(w1 @ f + b1, 0.0)
+        scores[i] = 1.0 / (1.0 + np.exp(-(w2 @ z + b2)))
+    return scores
+
+
+def coverage_at_k(pred_scores, routed_counts, k: int):
+    """Mass-weighted Coverage@k (section VI-B): routed token mass on the top-k predicted experts."""
+    pred_scores = np.asarray(pred_scores, dtype=np.float64)
+    routed_counts = np.asarray(routed_counts, dtype=np.float64)
+    order = np.lexsort((np.arange(pred_scores.size), -pred_scores))[:k]
+    total = routed_counts.sum()
+    return 0.0 if total == 0 else routed_counts[order].sum() / total
