@@ -1,0 +1,234 @@
+/*
+ * mira.h - C ABI of the Mira per-layer MoE expert step on AMD Instinct MI355X
+ * (gfx950).
+ *
+ * Paper: "Memory-Efficient MoE Inference Using Adaptive Caching and
+ * Predictive Expert Staging" (Mira).  The library runs one MoE layer over
+ * experts held in the paper's compressed expert format (section IV-B): router
+ * top-k and combine weights (section II-A), a stable token-to-expert
+ * permutation, the SwiGLU expert FFN fused with INT8 dequantization
+ * (sections IV-A and IV-F), and the weighted combine.  Experts are found
+ * through a slot table into a caller-owned pool of device slots, the HOT and
+ * STAGE regions of the expert cache (section IV-C); slots are filled from
+ * pinned host memory by asynchronous copies (sections IV-E, IV-F).  A small
+ * predictor head scores the experts of layer l+2 (section IV-E).
+ *
+ * Conventions for every entry point:
+ *  - Return 0 (MIRA_OK) on success or a negative mira_status.  A failing call
+ *    launches nothing; mira_last_error() then describes the failure (a
+ *    thread-local string owned by the library, valid until the next call on
+ *    the same thread).  No C++ exception crosses this interface.
+ *  - "device" pointers are HIP device allocations of the current device;
+ *    "host" pointers are ordinary host memory.  The caller owns every buffer;
+ *    the library never frees caller memory and allocates none on the forward
+ *    path (it uses the caller's workspace).
+ *  - Work is enqueued on the given HIP stream and is asynchronous: outputs are
+ *    valid once the stream reaches the call.  Only the host path of
+ *    mira_pack_experts runs synchronously.  Calls on distinct workspaces may
+ *    run concurrently.
+ *  - Tensors are dense and row-major; shapes are given in brackets.
+ */
+#ifndef MIRA_H_
+#define MIRA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------- */
+typedef enum mira_status {
+  MIRA_OK = 0,
+  MIRA_ERR_ARG = -1,        /* null pointer, bad enum or flag, inconsistent argument */
+  MIRA_ERR_SHAPE = -2,      /* unsupported or inconsistent sizes */
+  MIRA_ERR_ALIGN = -3,      /* a pointer or stride breaks the stated alignment */
+  MIRA_ERR_WORKSPACE = -4,  /* workspace missing or smaller than mira_workspace_bytes() */
+  MIRA_ERR_HIP = -5,        /* a HIP runtime call failed; the message names it */
+  MIRA_ERR_UNSUPPORTED = -6 /* valid request this build does not implement */
+} mira_status;
+
+/* ---- element types ------------------------------------------------------ */
+typedef enum mira_dtype {
+  MIRA_F32 = 0,  /* IEEE binary32 */
+  MIRA_BF16 = 1  /* bfloat16 (upper half of a binary32) */
+} mira_dtype;
+
+/* ---- flags of mira_shape.flags ------------------------------------------ */
+/* Combine weights are, by default, a softmax over the k selected router
+ * logits (renormalised top-k).  With this flag: softmax over all E logits,
+ * keeping the k selected probabilities. */
+#define MIRA_FLAG_SOFTMAX_ALL 0x1u
+/* Force the small-batch (decode) expert kernels; needs n_tokens <= MIRA_DECODE_MAX_TOKENS. */
+#define MIRA_FLAG_FORCE_DECODE 0x2u
+/* Force the grouped-GEMM (prefill) expert kernels for any n_tokens. */
+#define MIRA_FLAG_FORCE_PREFILL 0x4u
+
+/* Without a FORCE flag, calls with n_tokens <= this use the decode kernels. */
+#define MIRA_DECODE_MAX_TOKENS 16
+
+/* Size limits of this build. */
+#define MIRA_MAX_EXPERTS 256 /* n_experts + n_shared */
+#define MIRA_MAX_TOPK 16
+
+/* ---- packed expert format (section IV-B) --------------------------------
+ * One blob per expert, little-endian, at offsets
+ *   0       int8  gate [R][C]   (the matrix that goes through SiLU)
+ *   R*C     int8  up   [R][C]   (the linear branch)
+ *   2*R*C   int8  down [C][R]
+ *   3*R*C   bf16  sigma[R]      (one scale per expert-hidden row r, shared by
+ *                                gate row r, up row r and down column r)
+ * zero-padded to a multiple of 256 bytes.  The dequantized weights are
+ * sigma[r] * q.  Pack computes, per row r,
+ *   alpha_r = max(|gate[r,:]|_inf, |up[r,:]|_inf, |down[:,r]|_inf)  (exact),
+ *   s_r     = fl32(max(alpha_r, eps) / 127),
+ *   sigma_r = s_r rounded to bf16 (nearest, ties to even),
+ *   q       = clamp(rint_even(fl32(w / sigma_r)), -127, 127),
+ * with correctly rounded fp32 division; the integers are made against the
+ * stored sigma_r. */
+
+/* Size of one packed expert: 3*R*C + 2*R rounded up to a multiple of 256.
+ * Returns 0 if hidden or ffn is not positive or the size overflows. */
+size_t mira_packed_expert_bytes(int32_t hidden, int32_t ffn);
+
+/* Shape of one MoE layer. */
+typedef struct mira_shape {
+  int32_t hidden;    /* C: model hidden size; multiple of 64 */
+  int32_t ffn;       /* R: expert hidden size; multiple of 64 */
+  int32_t n_experts; /* E: routed experts, >= 1 */
+  int32_t top_k;     /* k: experts per token, 1 <= k <= min(E, MIRA_MAX_TOPK) */
+  int32_t n_shared;  /* S: shared experts applied to every token with weight 1, >= 0 */
+  int32_t act_dtype; /* mira_dtype of x and of the router weights */
+  uint32_t flags;    /* MIRA_FLAG_* */
+  int32_t reserved;  /* must be 0 */
+} mira_shape;
+
+/* Offline packing of experts into the format above (section IV-B; the
+ * paper converts all expert weights offline).
+ *   w_gate, w_up: [n_experts][R][C]; w_down: [n_experts][C][R]; element type
+ *     w_dtype (MIRA_F32 or MIRA_BF16; bf16 is widened exactly), finite values.
+ *   packed: [n_experts][packed_stride] bytes; packed_stride is a multiple of
+ *     256 and >= mira_packed_expert_bytes(C, R).  Padding bytes are zeroed.
+ *   eps: the paper's small constant (positive, finite), e.g. 1e-8.
+ *   on_device = 0: host pointers; runs on host threads and returns when done
+ *     (stream ignored).  on_device = 1: device pointers; enqueued on stream.
+ * Both paths produce identical bytes.  Only s->hidden and s->ffn are read. */
+int mira_pack_experts(const mira_shape* s, int32_t n_experts, int32_t w_dtype,
+                      const void* w_gate, const void* w_up, const void* w_down,
+                      float eps, void* packed, uint64_t packed_stride,
+                      int32_t on_device, hipStream_t stream);
+
+/* Arguments of one MoE-layer call; all pointers are device pointers. */
+typedef struct mira_moe_args {
+  const void* x;             /* [T][C] act_dtype, 16-byte aligned */
+  int32_t n_tokens;          /* T >= 0 (T = 0 is a no-op) */
+  int32_t n_slots;           /* number of slots in slot_pool */
+  const void* w_router;      /* [E][C] act_dtype, 16-byte aligned */
+  const float* router_bias;  /* [E] fp32, or NULL for no bias */
+  const int32_t* slot_table; /* [E+S]: slot holding each expert (routed
+                                experts first, then shared), or -1 when the
+                                expert is not resident */
+  const void* slot_pool;     /* n_slots * slot_stride bytes of packed experts */
+  uint64_t slot_stride;      /* multiple of 256, >= mira_packed_expert_bytes(C, R) */
+  float* out;                /* [T][C] fp32: sum_j w[t,j] * expert_{idx[t,j]}(x_t)
+                                plus the shared experts' outputs */
+  int32_t* topk_idx;         /* optional [T][k]: selected experts, best first */
+  float* topk_weight;        /* optional [T][k]: their combine weights */
+  float* logits;             /* optional [T][E]: fp32 router logits */
+  int32_t* expert_counts;    /* optional [E+S]: tokens routed to each expert */
+  int32_t* status;           /* optional single int32, set by the kernels:
+                                bit 0 = a selected expert had slot -1 (its
+                                contribution is missing from out),
+                                bit 1 = a slot index was >= n_slots (ignored) */
+  int32_t* expert_offsets;   /* optional [E+S+1]: start of each expert's group in
+                                the permuted pair order (exclusive scan of counts) */
+  int32_t* pair_order;       /* optional [T*k + S*T]: pair_order[pos] = pair at
+                                position pos of the permuted order; routed pair
+                                t*k+j, shared pair T*k + s*T + t; groups follow
+                                expert order, pairs inside a group increase */
+  void* workspace;           /* mira_workspace_bytes(s, max_tokens) bytes, 256-byte aligned */
+  uint64_t workspace_bytes;
+} mira_moe_args;
+
+/* Workspace needed by calls with up to max_tokens tokens (both paths). */
+size_t mira_workspace_bytes(const mira_shape* s, int32_t max_tokens);
+
+/* One MoE layer (section II-A; expert step of sections IV-A, IV-F):
+ * router logits l = x Wg^T + b (fp32 accumulate), top-k (value descending,
+ * lower index on ties), combine weights, stable grouping of (token, slot)
+ * pairs by expert, SwiGLU expert FFN on the packed experts fetched through
+ * slot_table, weighted combine into out.  Reads status-free inputs only;
+ * writes out and the optional outputs.  Deterministic: repeated calls on the
+ * same inputs give bit-identical results. */
+int mira_moe_forward(const mira_shape* s, const mira_moe_args* a, hipStream_t stream);
+
+/* The same call split in two so a runtime can fetch missing experts in
+ * between: mira_moe_route runs the router, top-k and permutation (writing the
+ * routing into the workspace and the optional outputs); mira_moe_experts then
+ * runs the expert FFN and combine for that routing.  Both calls must get the
+ * same shape, tokens and workspace; slot_table may change in between. */
+int mira_moe_route(const mira_shape* s, const mira_moe_args* a, hipStream_t stream);
+int mira_moe_experts(const mira_shape* s, const mira_moe_args* a, hipStream_t stream);
+
+/* ---- predictor head (section IV-E) -------------------------------------- */
+typedef struct mira_pred_shape {
+  int32_t hidden;      /* C; multiple of 64 */
+  int32_t pred_hidden; /* P: hidden width of the MLP, >= 1 */
+  int32_t n_out;       /* experts scored for layer l+2, 1..MIRA_MAX_EXPERTS */
+  int32_t group;       /* token rows mean-pooled per evaluation, >= 1 */
+  int32_t act_dtype;   /* mira_dtype of x */
+  int32_t reserved;    /* must be 0 */
+} mira_pred_shape;
+
+/* Bytes of workspace mira_predict needs for n_tokens tokens. */
+size_t mira_predict_workspace_bytes(const mira_pred_shape* p, int32_t n_tokens);
+
+/* Scores of layer l+2's experts from layer l's hidden states:
+ *   f_i = mean of rows [i*group, (i+1)*group) of x,
+ *   z   = ReLU(W1 f_i + b1),  scores[i] = sigmoid(W2 z + b2),
+ * fp32 accumulation.  x [T][C] (act_dtype), T a multiple of group;
+ * w1 [P][C] bf16; b1 [P] fp32 or NULL; w2 [n_out][P] bf16; b2 [n_out] fp32 or
+ * NULL; scores [T/group][n_out] fp32.  All device pointers. */
+int mira_predict(const mira_pred_shape* p, const void* x, int32_t n_tokens,
+                 const void* w1, const float* b1, const void* w2, const float* b2,
+                 float* scores, void* workspace, uint64_t workspace_bytes,
+                 hipStream_t stream);
+
+/* ---- expert staging (sections IV-C, IV-E, IV-F) ------------------------- */
+/* Copy one packed expert from pinned host memory into slot `slot` of a slot
+ * pool with hipMemcpyAsync on copy_stream, then record `done` (if not NULL)
+ * on copy_stream.  bytes <= slot_stride; pinned_src must be page-locked host
+ * memory.  The caller makes the compute stream wait on `done` before any
+ * kernel reads the slot. */
+int mira_stage_expert(void* slot_pool, uint64_t slot_stride, int32_t slot,
+                      const void* pinned_src, uint64_t bytes,
+                      hipStream_t copy_stream, hipEvent_t done);
+
+/* Write slot_table[expert] = slot with a one-thread kernel on `stream`
+ * (stream-ordered, so a later forward call on the stream sees it). */
+int mira_set_slot(int32_t* slot_table, int32_t expert, int32_t slot, hipStream_t stream);
+
+/* ---- diagnostics -------------------------------------------------------- */
+/* Description of the last failure on this thread ("" if none). */
+const char* mira_last_error(void);
+
+/* Library version string. */
+const char* mira_version(void);
+
+/* Kernel timing for measurement.  While enabled, every kernel the library
+ * launches is bracketed by a pair of HIP events recorded on its stream;
+ * mira_profile_read synchronises on them and reports, per kernel name, the
+ * launch count and the summed duration in milliseconds, then clears the
+ * records.  Names are library-owned strings. */
+int mira_profile_enable(int32_t enable);
+int mira_profile_read(int32_t max_entries, const char** names, int32_t* counts,
+                      double* total_ms, int32_t* n_entries);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MIRA_H_ */

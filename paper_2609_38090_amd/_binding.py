@@ -1,0 +1,264 @@
+"""ctypes binding of libmira.so: argument marshalling only."""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+from dataclasses import dataclass, field, fields
+from typing import Any, Optional
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+_LIB_NAME = "libmira.so"
+
+MIRA_F32 = 0
+MIRA_BF16 = 1
+MIRA_FLAG_SOFTMAX_ALL = 0x1
+MIRA_FLAG_FORCE_DECODE = 0x2
+MIRA_FLAG_FORCE_PREFILL = 0x4
+MIRA_DECODE_MAX_TOKENS = 16
+MIRA_MAX_EXPERTS = 256
+MIRA_MAX_TOPK = 16
+
+
+class MiraError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"mira error {code}: {msg}")
+        self.code = code
+
+
+class _Shape(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("ffn", ctypes.c_int32), ("n_experts", ctypes.c_int32),
+                ("top_k", ctypes.c_int32), ("n_shared", ctypes.c_int32), ("act_dtype", ctypes.c_int32),
+                ("flags", ctypes.c_uint32), ("reserved", ctypes.c_int32)]
+
+
+class _Args(ctypes.Structure):
+    _fields_ = [("x", ctypes.c_void_p), ("n_tokens", ctypes.c_int32), ("n_slots", ctypes.c_int32),
+                ("w_router", ctypes.c_void_p), ("router_bias", ctypes.c_void_p),
+                ("slot_table", ctypes.c_void_p), ("slot_pool", ctypes.c_void_p),
+                ("slot_stride", ctypes.c_uint64), ("out", ctypes.c_void_p),
+                ("topk_idx", ctypes.c_void_p), ("topk_weight", ctypes.c_void_p),
+                ("logits", ctypes.c_void_p), ("expert_counts", ctypes.c_void_p),
+                ("status", ctypes.c_void_p), ("expert_offsets", ctypes.c_void_p),
+                ("pair_order", ctypes.c_void_p), ("workspace", ctypes.c_void_p),
+                ("workspace_bytes", ctypes.c_uint64)]
+
+
+class _PredShape(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("pred_hidden", ctypes.c_int32), ("n_out", ctypes.c_int32),
+                ("group", ctypes.c_int32), ("act_dtype", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+@dataclass
+class MoEShape:
+    """mira_shape: C (hidden), R (ffn), E, k, S, activation dtype and flags."""
+    hidden: int
+    ffn: int
+    n_experts: int
+    top_k: int
+    n_shared: int = 0
+    act_dtype: int = MIRA_BF16
+    flags: int = 0
+
+    def _c(self) -> _Shape:
+        return _Shape(self.hidden, self.ffn, self.n_experts, self.top_k, self.n_shared,
+                      self.act_dtype, self.flags, 0)
+
+
+@dataclass
+class PredShape:
+    """mira_pred_shape: C, P (MLP width), scored experts, pooled rows per evaluation."""
+    hidden: int
+    pred_hidden: int
+    n_out: int
+    group: int
+    act_dtype: int = MIRA_BF16
+
+    def _c(self) -> _PredShape:
+        return _PredShape(self.hidden, self.pred_hidden, self.n_out, self.group, self.act_dtype, 0)
+
+
+@dataclass
+class MoEArgs:
+    """mira_moe_args.  Pointer fields take torch tensors, integer addresses or None."""
+    x: Any = None
+    n_tokens: int = 0
+    n_slots: int = 0
+    w_router: Any = None
+    router_bias: Any = None
+    slot_table: Any = None
+    slot_pool: Any = None
+    slot_stride: int = 0
+    out: Any = None
+    topk_idx: Any = None
+    topk_weight: Any = None
+    logits: Any = None
+    expert_counts: Any = None
+    status: Any = None
+    expert_offsets: Any = None
+    pair_order: Any = None
+    workspace: Any = None
+    workspace_bytes: int = 0
+
+    def _c(self) -> _Args:
+        vals = {}
+        for f in fields(self):
+            v = getattr(self, f.name)
+            vals[f.name] = v if f.name in ("n_tokens", "n_slots", "slot_stride", "workspace_bytes") else _ptr(v)
+        return _Args(**vals)
+
+
+def _ptr(v) -> Optional[int]:
+    if v is None:
+        return None
+    if isinstance(v, int):
+        return v or None
+    if hasattr(v, "data_ptr"):
+        return v.data_ptr() or None
+    raise TypeError(f"cannot take the address of {type(v).__name__}")
+
+
+def _stream(s) -> Optional[int]:
+    if s is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream or None
+    if isinstance(s, int):
+        return s or None
+    if hasattr(s, "cuda_stream"):
+        return s.cuda_stream or None
+    raise TypeError("stream must be a torch stream, an integer hipStream_t or None")
+
+
+_LIB = None
+_LOCK = threading.Lock()
+
+
+def lib_path() -> str:
+    return os.path.join(_PKG, _LIB_NAME)
+
+
+def load():
+    """Load libmira.so (after torch, so both share torch's HIP runtime)."""
+    global _LIB
+    with _LOCK:
+        if _LIB is not None:
+            return _LIB
+        path = lib_path()
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is not built; run paper_2609_38090_amd.build.build() first")
+        import torch  # noqa: F401  (loads the HIP runtime the library binds to)
+        lib = ctypes.CDLL(path)
+        vp, i32, u32, u64, f32, sz = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32,
+                                      ctypes.c_uint64, ctypes.c_float, ctypes.c_size_t)
+        sig = {
+            "mira_packed_expert_bytes": (sz, [i32, i32]),
+            "mira_workspace_bytes": (sz, [ctypes.POINTER(_Shape), i32]),
+            "mira_pack_experts": (ctypes.c_int, [ctypes.POINTER(_Shape), i32, i32, vp, vp, vp, f32, vp,
+                                                 u64, i32, vp]),
+            "mira_moe_forward": (ctypes.c_int, [ctypes.POINTER(_Shape), ctypes.POINTER(_Args), vp]),
+            "mira_moe_route": (ctypes.c_int, [ctypes.POINTER(_Shape), ctypes.POINTER(_Args), vp]),
+            "mira_moe_experts": (ctypes.c_int, [ctypes.POINTER(_Shape), ctypes.POINTER(_Args), vp]),
+            "mira_predict_workspace_bytes": (sz, [ctypes.POINTER(_PredShape), i32]),
+            "mira_predict": (ctypes.c_int, [ctypes.POINTER(_PredShape), vp, i32, vp, vp, vp, vp, vp, vp,
+                                            u64, vp]),
+            "mira_stage_expert": (ctypes.c_int, [vp, u64, i32, vp, u64, vp, vp]),
+            "mira_set_slot": (ctypes.c_int, [vp, i32, i32, vp]),
+            "mira_last_error": (ctypes.c_char_p, []),
+            "mira_version": (ctypes.c_char_p, []),
+            "mira_profile_enable": (ctypes.c_int, [i32]),
+            "mira_profile_read": (ctypes.c_int, [i32, ctypes.POINTER(ctypes.c_char_p),
+                                                 ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double),
+                                                 ctypes.POINTER(i32)]),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        del u32
+        _LIB = lib
+        return lib
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise MiraError(rc, mira_last_error())
+
+
+# ---- entry points (names of the C ABI) -------------------------------------
+
+def mira_last_error() -> str:
+    return load().mira_last_error().decode()
+
+
+def mira_version() -> str:
+    return load().mira_version().decode()
+
+
+def mira_packed_expert_bytes(hidden: int, ffn: int) -> int:
+    return int(load().mira_packed_expert_bytes(hidden, ffn))
+
+
+def mira_workspace_bytes(shape: MoEShape, max_tokens: int) -> int:
+    n = int(load().mira_workspace_bytes(ctypes.byref(shape._c()), max_tokens))
+    if n == 0:
+        raise MiraError(-1, "invalid shape for mira_workspace_bytes")
+    return n
+
+
+def mira_pack_experts(shape: MoEShape, n_experts: int, w_dtype: int, w_gate, w_up, w_down,
+                      eps: float, packed, packed_stride: int, on_device: int, stream=None):
+    st = _stream(stream) if on_device else None
+    _check(load().mira_pack_experts(ctypes.byref(shape._c()), n_experts, w_dtype, _ptr(w_gate),
+                                    _ptr(w_up), _ptr(w_down), eps, _ptr(packed), packed_stride,
+                                    on_device, st))
+
+
+def mira_moe_forward(shape: MoEShape, args: MoEArgs, stream=None):
+    _check(load().mira_moe_forward(ctypes.byref(shape._c()), ctypes.byref(args._c()), _stream(stream)))
+
+
+def mira_moe_route(shape: MoEShape, args: MoEArgs, stream=None):
+    _check(load().mira_moe_route(ctypes.byref(shape._c()), ctypes.byref(args._c()), _stream(stream)))
+
+
+def mira_moe_experts(shape: MoEShape, args: MoEArgs, stream=None):
+    _check(load().mira_moe_experts(ctypes.byref(shape._c()), ctypes.byref(args._c()), _stream(stream)))
+
+
+def mira_predict_workspace_bytes(pshape: PredShape, n_tokens: int) -> int:
+    return int(load().mira_predict_workspace_bytes(ctypes.byref(pshape._c()), n_tokens))
+
+
+def mira_predict(pshape: PredShape, x, n_tokens: int, w1, b1, w2, b2, scores, workspace,
+                 workspace_bytes: int, stream=None):
+    _check(load().mira_predict(ctypes.byref(pshape._c()), _ptr(x), n_tokens, _ptr(w1), _ptr(b1),
+                               _ptr(w2), _ptr(b2), _ptr(scores), _ptr(workspace), workspace_bytes,
+                               _stream(stream)))
+
+
+def mira_stage_expert(slot_pool, slot_stride: int, slot: int, pinned_src, nbytes: int,
+                      copy_stream=None, done_event=None):
+    ev = None
+    if done_event is not None:
+        ev = done_event if isinstance(done_event, int) else done_event.cuda_event
+    _check(load().mira_stage_expert(_ptr(slot_pool), slot_stride, slot, _ptr(pinned_src), nbytes,
+                                    _stream(copy_stream), ev))
+
+
+def mira_set_slot(slot_table, expert: int, slot: int, stream=None):
+    _check(load().mira_set_slot(_ptr(slot_table), expert, slot, _stream(stream)))
+
+
+def mira_profile_enable(enable: bool = True):
+    _check(load().mira_profile_enable(1 if enable else 0))
+
+
+def mira_profile_read(max_entries: int = 64):
+    """{kernel name: (launches, total ms)} since the last read."""
+    lib = load()
+    names = (ctypes.c_char_p * max_entries)()
+    counts = (ctypes.c_int32 * max_entries)()
+    ms = (ctypes.c_double * max_entries)()
+    n = ctypes.c_int32(0)
+    _check(lib.mira_profile_read(max_entries, names, counts, ms, ctypes.byref(n)))
+    return {names[i].decode(): (int(counts[i]), float(ms[i])) for i in range(min(n.value, max_entries))}

@@ -1,0 +1,337 @@
+// Small-batch (decode) expert FFN over packed experts.
+//
+// The paper fuses INT8 dequantization into the expert FFN (sections IV-A and
+// IV-F).  Because the scale sigma_r is shared by gate row r, up row r and down
+// column r (section IV-B), it factors out of every dot product:
+//   G = sigma (.) (Qg x),  U = sigma (.) (Qu x),  H' = sigma (.) silu(G) (.) U,
+//   y = Qd H'.
+// With one to a few tokens per expert the step is bound by streaming the
+// packed int8 bytes from HBM.  These kernels feed those bytes unchanged to the
+// int8 matrix cores (v_mfma_i32_16x16x64_i8): the activation side is written
+// as a fixed-point integer split into three signed base-256 digits, each digit
+// one int8 operand column, so the products and sums are exact int32 and the
+// only rounding is the fixed-point step (relative 2^-22 of the row or block
+// maximum) and the final fp32 arithmetic.  Five tokens (15 digit columns) fit
+// one 16-column operand.
+#include "device_util.h"
+#include "mira_internal.h"
+
+namespace mira {
+
+// ---------------------------------------------------------------------------
+// Per-token fixed-point digits of x: |x * 2^E_t| < 2^22, E_t from max_c |x[t,c]|.
+// Layout: xdig[(t*3 + d)*C + c], xexp[t] = E_t.
+// ---------------------------------------------------------------------------
+template <typename ActT>
+__global__ __launch_bounds__(256) void digitize_x_kernel(const ActT* __restrict__ x, int C,
+                                                         int8_t* __restrict__ xdig,
+                                                         int32_t* __restrict__ xexp) {
+  __shared__ float red[4];
+  const int t = blockIdx.x, tid = threadIdx.x;
+  const ActT* xr = x + (size_t)t * C;
+  float m = 0.f;
+  for (int c = tid; c < C; c += 256) m = fmaxf(m, fabsf(load_act(xr, c)));
+  m = wave_max(m);
+  if ((tid & 63) == 0) red[tid >> 6] = m;
+  __syncthreads();
+  m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  const int E = kFixBits - exp_bound(m);
+  int8_t* d0p = xdig + (size_t)t * kDigits * C;
+  for (int c = tid; c < C; c += 256) {
+    const int v = (int)rintf(ldexpf(load_act(xr, c), E));
+    int d0, d1, d2;
+    split_digits(v, d0, d1, d2);
+    d0p[c] = (int8_t)d0;
+    d0p[C + c] = (int8_t)d1;
+    d0p[2 * C + c] = (int8_t)d2;
+  }
+  if (tid == 0) xexp[t] = E;
+}
+
+// Combine the three digit columns held by lanes j, j+1, j+2 (j = 3m) into
+// the exact integer dot product.
+__device__ __forceinline__ float combine_digits_i(int s0) {
+  const int s1 = __shfl_down(s0, 1, 64);
+  const int s2 = __shfl_down(s0, 2, 64);
+  const long long v = (long long)s2 * 65536 + (long long)s1 * 256 + (long long)s0;
+  return (float)v;
+}
+
+// ---------------------------------------------------------------------------
+// Gate/up + SwiGLU.  Workgroup = (non-empty expert a, block of 64 rows of R);
+// wave w owns 16 rows.  Writes H' as per-block fixed-point digits:
+// hdig[(pos*3 + d)*R + r], hexp[pos*(R/64) + rb].
+// ---------------------------------------------------------------------------
+constexpr int kDecUnroll = 4;
+
+template <int NG>
+__global__ __launch_bounds__(256) void decode_gateup_kernel(
+    int C, int R, ExpertPool ep, const int32_t* __restrict__ misc,
+    const int32_t* __restrict__ active, const int32_t* __restrict__ offsets,
+    const int32_t* __restrict__ tokpos, const int8_t* __restrict__ xdig,
+    const int32_t* __restrict__ xexp, int8_t* __restrict__ hdig, int32_t* __restrict__ hexp) {
+  __shared__ float bmax[4][NG * kTokPerGroup];
+  const int nrb = R / kBlk;
+  const int a = blockIdx.x / nrb, rb = blockIdx.x - a * nrb;
+  if (a >= misc[MISC_NACTIVE]) return;
+  const int g = active[a];
+  const int off = offsets[g], n = offsets[g + 1] - off;
+  const int slot = ep.slot_table[g];
+  if (slot < 0 || slot >= ep.n_slots) {
+    if (threadIdx.x == 0 && ep.status) atomicOr(ep.status, slot < 0 ? 1 : 2);
+    return;
+  }
+  const int8_t* blob = ep.pool + (size_t)slot * ep.stride;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kg = lane >> 4;
+  const int row = rb * kBlk + wave * 16 + r16;
+  const int8_t* gp = blob + (size_t)row * C + kg * 16;
+  const int8_t* up = gp + (size_t)R * C;
+
+  const int m = r16 / 3, d = r16 - 3 * m;
+  const int8_t* bp[NG];
+  bool bv[NG];
+  int tokv[NG];
+#pragma unroll
+  for (int cg = 0; cg < NG; ++cg) {
+    const int i = cg * kTokPerGroup + m;
+    bv[cg] = r16 < 3 * kTokPerGroup && i < n;
+    tokv[cg] = bv[cg] ? tokpos[off + i] : 0;
+    bp[cg] = xdig + ((size_t)tokv[cg] * kDigits + d) * C + kg * 16;
+  }
+
+  v4i accg[NG], accu[NG];
+#pragma unroll
+  for (int cg = 0; cg < NG; ++cg) accg[cg] = accu[cg] = zero16();
+
+  const int nks = C / 64;
+  int ks = 0;
+  for (; ks + kDecUnroll <= nks; ks += kDecUnroll) {
+    v4i ag[kDecUnroll], au[kDecUnroll], bb[kDecUnroll][NG];
+#pragma unroll
+    for (int u = 0; u < kDecUnroll; ++u) {
+      ag[u] = ld16_stream(gp + (ks + u) * 64);
+      au[u] = ld16_stream(up + (ks + u) * 64);
+#pragma unroll
+      for (int cg = 0; cg < NG; ++cg) bb[u][cg] = bv[cg] ? ld16(bp[cg] + (ks + u) * 64) : zero16();
+    }
+#pragma unroll
+    for (int u = 0; u < kDecUnroll; ++u)
+#pragma unroll
+      for (int cg = 0; cg < NG; ++cg) {
+        accg[cg] = mfma_i8(ag[u], bb[u][cg], accg[cg]);
+        accu[cg] = mfma_i8(au[u], bb[u][cg], accu[cg]);
+      }
+  }
+  for (; ks < nks; ++ks) {
+    const v4i ag = ld16_stream(gp + ks * 64), au = ld16_stream(up + ks * 64);
+#pragma unroll
+    for (int cg = 0; cg < NG; ++cg) {
+      const v4i b = bv[cg] ? ld16(bp[cg] + ks * 64) : zero16();
+      accg[cg] = mfma_i8(ag, b, accg[cg]);
+      accu[cg] = mfma_i8(au, b, accu[cg]);
+    }
+  }
+
+  // epilogue: rows rbase+i (i < 4) for token column r16
+  const int rbase = rb * kBlk + wave * 16 + kg * 4;
+  const uint16_t* sig = (const uint16_t*)(blob + (size_t)3 * R * C);
+  float sg[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) sg[i] = bf16_to_f32(sig[rbase + i]);
+  const bool lead = d == 0;
+  float hv[NG][4];
+#pragma unroll
+  for (int cg = 0; cg < NG; ++cg) {
+    const float xs = bv[cg] ? ldexpf(1.f, -xexp[tokv[cg]]) : 0.f;
+    float mx = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float gsum = combine_digits_i(accg[cg][i]);
+      const float usum = combine_digits_i(accu[cg][i]);
+      const float gv = gsum * xs * sg[i];
+      const float uv = usum * xs * sg[i];
+      const float h = gv / (1.f + expf(-gv)) * uv;
+      hv[cg][i] = (lead && bv[cg]) ? sg[i] * h : 0.f;
+      mx = fmaxf(mx, fabsf(hv[cg][i]));
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    if (kg == 0 && lead && r16 < 3 * kTokPerGroup) bmax[wave][cg * kTokPerGroup + m] = mx;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int cg = 0; cg < NG; ++cg) {
+    if (!(lead && bv[cg])) continue;
+    const int ti = cg * kTokPerGroup + m;
+    const float mx = fmaxf(fmaxf(bmax[0][ti], bmax[1][ti]), fmaxf(bmax[2][ti], bmax[3][ti]));
+    const int Eh = kFixBits - exp_bound(mx);
+    uint32_t w0 = 0, w1 = 0, w2 = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int v = (int)rintf(ldexpf(hv[cg][i], Eh));
+      int d0, d1, d2;
+      split_digits(v, d0, d1, d2);
+      w0 |= (uint32_t)(d0 & 0xFF) << (8 * i);
+      w1 |= (uint32_t)(d1 & 0xFF) << (8 * i);
+      w2 |= (uint32_t)(d2 & 0xFF) << (8 * i);
+    }
+    const size_t pos = (size_t)off + ti;
+    int8_t* hp = hdig + pos * kDigits * R + rbase;
+    *(uint32_t*)(hp) = w0;
+    *(uint32_t*)(hp + R) = w1;
+    *(uint32_t*)(hp + 2 * (size_t)R) = w2;
+    if (wave == 0 && kg == 0) hexp[pos * nrb + rb] = Eh;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Down projection + weighted combine.  Workgroup = 16 output rows c; its KS
+// waves split the R dimension.  For every non-empty expert, y = Qd H' with
+// per-64-row exponents of H', multiplied by the combine weight of each
+// (token, expert) pair and summed per token in a fixed order (expert list
+// order inside a wave, then wave order), so the result is deterministic.
+// ---------------------------------------------------------------------------
+template <int NG, int KS>
+__global__ __launch_bounds__(64 * KS) void decode_down_kernel(
+    int C, int R, int T, ExpertPool ep, const int32_t* __restrict__ misc,
+    const int32_t* __restrict__ active, const int32_t* __restrict__ offsets,
+    const int32_t* __restrict__ tokpos, const float* __restrict__ wpos,
+    const int8_t* __restrict__ hdig, const int32_t* __restrict__ hexp, float* __restrict__ out) {
+  __shared__ float part[KS][MIRA_DECODE_MAX_TOKENS][16];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  for (int i = tid; i < KS * MIRA_DECODE_MAX_TOKENS * 16; i += 64 * KS) (&part[0][0][0])[i] = 0.f;
+  __syncthreads();
+
+  const int c0 = blockIdx.x * 16;
+  const int r16 = lane & 15, kg = lane >> 4;
+  const int m = r16 / 3, d = r16 - 3 * m;
+  const int nks = R / 64;
+  const int spw = (nks + KS - 1) / KS;
+  const int ks_beg = wave * spw, ks_end = min(nks, ks_beg + spw);
+  const int na = misc[MISC_NACTIVE];
+
+  for (int a = 0; a < na; ++a) {
+    const int g = active[a];
+    const int off = offsets[g], n = offsets[g + 1] - off;
+    const int slot = ep.slot_table[g];
+    if (slot < 0 || slot >= ep.n_slots) continue;
+    const int8_t* dp = ep.pool + (size_t)slot * ep.stride + (size_t)2 * R * C +
+                       (size_t)(c0 + r16) * R + kg * 16;
+    const int8_t* bp[NG];
+    const int32_t* hx[NG];
+    bool bv[NG];
+#pragma unroll
+    for (int cg = 0; cg < NG; ++cg) {
+      const int i = cg * kTokPerGroup + m;
+      bv[cg] = r16 < 3 * kTokPerGroup && i < n;
+      const size_t pos = (size_t)off + (bv[cg] ? i : 0);
+      bp[cg] = hdig + (pos * kDigits + d) * R + kg * 16;
+      hx[cg] = hexp + pos * nks;
+    }
+    float facc[NG][4];
+#pragma unroll
+    for (int cg = 0; cg < NG; ++cg)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) facc[cg][i] = 0.f;
+
+    int ks = ks_beg;
+    for (; ks + kDecUnroll <= ks_end; ks += kDecUnroll) {
+      v4i av[kDecUnroll], bb[kDecUnroll][NG];
+      int he[kDecUnroll][NG];
+#pragma unroll
+      for (int u = 0; u < kDecUnroll; ++u) {
+        av[u] = ld16_stream(dp + (ks + u) * 64);
+#pragma unroll
+        for (int cg = 0; cg < NG; ++cg) {
+          bb[u][cg] = bv[cg] ? ld16(bp[cg] + (ks + u) * 64) : zero16();
+          he[u][cg] = bv[cg] ? hx[cg][ks + u] : 0;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kDecUnroll; ++u)
+#pragma unroll
+        for (int cg = 0; cg < NG; ++cg) {
+          const v4i s = mfma_i8(av[u], bb[u][cg], zero16());
+          const float sc = bv[cg] ? ldexpf(1.f, 8 * d - he[u][cg]) : 0.f;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) facc[cg][i] = fmaf((float)s[i], sc, facc[cg][i]);
+        }
+    }
+    for (; ks < ks_end; ++ks) {
+      const v4i av = ld16_stream(dp + ks * 64);
+#pragma unroll
+      for (int cg = 0; cg < NG; ++cg) {
+        const v4i b = bv[cg] ? ld16(bp[cg] + ks * 64) : zero16();
+        const v4i s = mfma_i8(av, b, zero16());
+        const float sc = bv[cg] ? ldexpf(1.f, 8 * d - hx[cg][ks]) : 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) facc[cg][i] = fmaf((float)s[i], sc, facc[cg][i]);
+      }
+    }
+#pragma unroll
+    for (int cg = 0; cg < NG; ++cg) {
+      const int ti = cg * kTokPerGroup + m;
+      const bool lead = d == 0 && bv[cg];
+      const int t = lead ? tokpos[off + ti] : 0;
+      const float wgt = lead ? wpos[off + ti] : 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float v = facc[cg][i] + __shfl_down(facc[cg][i], 1, 64) +
+                        __shfl_down(facc[cg][i], 2, 64);
+        if (lead) part[wave][t][kg * 4 + i] += wgt * v;
+      }
+    }
+  }
+  __syncthreads();
+  for (int i = tid; i < T * 16; i += 64 * KS) {
+    const int t = i >> 4, r = i & 15;
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < KS; ++w) s += part[w][t][r];
+    out[(size_t)t * C + c0 + r] = s;
+  }
+}
+
+constexpr int kDownKS = 8;
+
+template <int NG>
+static void launch_decode_ffn(const Layout& L, const WsPtr& w, const ExpertPool& ep, float* out,
+                              hipStream_t st) {
+  const int nrb = L.R / kBlk;
+  const int max_active = L.G < L.T * L.k + L.S ? L.G : L.T * L.k + L.S;
+  prof_begin("decode_gateup", st);
+  hipLaunchKernelGGL(decode_gateup_kernel<NG>, dim3(max_active * nrb), dim3(256), 0, st, L.C,
+                     L.R, ep, w.misc, w.active, w.offsets, w.tokpos, w.xdig, w.xexp, w.hdig,
+                     w.hexp);
+  prof_end("decode_gateup", st);
+  prof_begin("decode_down", st);
+  hipLaunchKernelGGL((decode_down_kernel<NG, kDownKS>), dim3(L.C / 16), dim3(64 * kDownKS), 0, st,
+                     L.C, L.R, L.T, ep, w.misc, w.active, w.offsets, w.tokpos, w.wpos, w.hdig,
+                     w.hexp, out);
+  prof_end("decode_down", st);
+}
+
+hipError_t launch_decode(const mira_shape& s, const Layout& L, const WsPtr& w, const void* x,
+                         const ExpertPool& ep, float* out, hipStream_t st) {
+  const int T = L.T;
+  if (T == 0) return hipSuccess;
+  prof_begin("decode_digitize", st);
+  if (s.act_dtype == MIRA_BF16)
+    hipLaunchKernelGGL(digitize_x_kernel<uint16_t>, dim3(T), dim3(256), 0, st,
+                       (const uint16_t*)x, L.C, w.xdig, w.xexp);
+  else
+    hipLaunchKernelGGL(digitize_x_kernel<float>, dim3(T), dim3(256), 0, st, (const float*)x, L.C,
+                       w.xdig, w.xexp);
+  prof_end("decode_digitize", st);
+  const int ng = (T + kTokPerGroup - 1) / kTokPerGroup;  // every group holds <= T tokens
+  switch (ng) {
+    case 1: launch_decode_ffn<1>(L, w, ep, out, st); break;
+    case 2: launch_decode_ffn<2>(L, w, ep, out, st); break;
+    case 3: launch_decode_ffn<3>(L, w, ep, out, st); break;
+    default: launch_decode_ffn<4>(L, w, ep, out, st); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace mira

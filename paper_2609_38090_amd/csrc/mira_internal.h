@@ -1,0 +1,170 @@
+// Internal declarations shared by the HIP kernels and the host entry points.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "mira.h"
+
+namespace mira {
+
+// ---------------------------------------------------------------------------
+// Compile-time tiling constants
+// ---------------------------------------------------------------------------
+constexpr int kDigits = 3;           // base-256 digits of a fixed-point activation
+constexpr int kFixBits = 22;         // |fixed-point value| < 2^22
+constexpr int kBlk = 64;             // rows of H' sharing one fixed-point exponent
+constexpr int kTokPerGroup = 5;      // tokens per 16-column MFMA operand (3 digits each)
+constexpr int kDecodeMaxGroups = (MIRA_DECODE_MAX_TOKENS + kTokPerGroup - 1) / kTokPerGroup;
+constexpr int kPrefBM = 64;          // prefill tile: tokens per m-tile (shared by both GEMMs)
+
+inline __host__ __device__ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// ---------------------------------------------------------------------------
+// Workspace layout of one call with T tokens.  Every region is 256-aligned.
+// Decode regions are sized for min(T, MIRA_DECODE_MAX_TOKENS) tokens.
+// ---------------------------------------------------------------------------
+struct Layout {
+  int T, E, S, G, k, C, R;
+  int P;        // (token, slot) pairs: T*k + S*T
+  int Pd;       // pairs of the decode sizing
+  int Td;       // tokens of the decode sizing
+  int mt_max;   // upper bound of prefill m-tiles
+  size_t logits, idx, wts, counts, offsets, inv, tokpos, wpos, misc, active, mstart, mtile_g,
+      mtile_m0, xdig, xexp, hdig, hexp, xb16, hbuf, ybuf, total;
+};
+
+// misc[] slots (int32)
+enum : int { MISC_NACTIVE = 0, MISC_MTOTAL = 1, MISC_COUNT = 16 };
+
+inline Layout make_layout(const mira_shape& s, int T) {
+  Layout L{};
+  L.T = T;
+  L.E = s.n_experts;
+  L.S = s.n_shared;
+  L.G = s.n_experts + s.n_shared;
+  L.k = s.top_k;
+  L.C = s.hidden;
+  L.R = s.ffn;
+  L.P = T * s.top_k + s.n_shared * T;
+  L.Td = T < MIRA_DECODE_MAX_TOKENS ? T : MIRA_DECODE_MAX_TOKENS;
+  L.Pd = L.Td * s.top_k + s.n_shared * L.Td;
+  L.mt_max = L.P / kPrefBM + L.G + 1;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o = align_up(o + bytes, 256);
+    return at;
+  };
+  const size_t P = (size_t)L.P, G = (size_t)L.G, Tz = (size_t)T;
+  L.logits = take(Tz * L.E * 4);
+  L.idx = take(Tz * L.k * 4);
+  L.wts = take(Tz * L.k * 4);
+  L.counts = take(G * 4);
+  L.offsets = take((G + 1) * 4);
+  L.inv = take(P * 4);
+  L.tokpos = take(P * 4);
+  L.wpos = take(P * 4);
+  L.misc = take(MISC_COUNT * 4);
+  L.active = take(G * 4);
+  L.mstart = take((G + 1) * 4);
+  L.mtile_g = take((size_t)L.mt_max * 4);
+  L.mtile_m0 = take((size_t)L.mt_max * 4);
+  L.xdig = take((size_t)L.Td * kDigits * L.C);
+  L.xexp = take((size_t)L.Td * 4);
+  L.hdig = take((size_t)L.Pd * kDigits * L.R);
+  L.hexp = take((size_t)L.Pd * (L.R / kBlk) * 4);
+  L.xb16 = take(s.act_dtype == MIRA_F32 ? Tz * L.C * 2 : 0);
+  L.hbuf = take(P * L.R * 2);
+  L.ybuf = take(P * L.C * 4);
+  L.total = o;
+  return L;
+}
+
+// Device pointers of one call's workspace regions.
+struct WsPtr {
+  float* logits;
+  int32_t* idx;
+  float* wts;
+  int32_t* counts;
+  int32_t* offsets;
+  int32_t* inv;
+  int32_t* tokpos;
+  float* wpos;
+  int32_t* misc;
+  int32_t* active;
+  int32_t* mstart;
+  int32_t* mtile_g;
+  int32_t* mtile_m0;
+  int8_t* xdig;
+  int32_t* xexp;
+  int8_t* hdig;
+  int32_t* hexp;
+  uint16_t* xb16;
+  uint16_t* hbuf;
+  float* ybuf;
+};
+
+inline WsPtr ws_ptrs(const Layout& L, void* base) {
+  char* b = (char*)base;
+  WsPtr w;
+  w.logits = (float*)(b + L.logits);
+  w.idx = (int32_t*)(b + L.idx);
+  w.wts = (float*)(b + L.wts);
+  w.counts = (int32_t*)(b + L.counts);
+  w.offsets = (int32_t*)(b + L.offsets);
+  w.inv = (int32_t*)(b + L.inv);
+  w.tokpos = (int32_t*)(b + L.tokpos);
+  w.wpos = (float*)(b + L.wpos);
+  w.misc = (int32_t*)(b + L.misc);
+  w.active = (int32_t*)(b + L.active);
+  w.mstart = (int32_t*)(b + L.mstart);
+  w.mtile_g = (int32_t*)(b + L.mtile_g);
+  w.mtile_m0 = (int32_t*)(b + L.mtile_m0);
+  w.xdig = (int8_t*)(b + L.xdig);
+  w.xexp = (int32_t*)(b + L.xexp);
+  w.hdig = (int8_t*)(b + L.hdig);
+  w.hexp = (int32_t*)(b + L.hexp);
+  w.xb16 = (uint16_t*)(b + L.xb16);
+  w.hbuf = (uint16_t*)(b + L.hbuf);
+  w.ybuf = (float*)(b + L.ybuf);
+  return w;
+}
+
+// Everything the expert kernels need to find a packed expert.
+struct ExpertPool {
+  const int8_t* pool;
+  const int32_t* slot_table;
+  uint64_t stride;
+  int32_t n_slots;
+  int32_t* status;  // may be null
+};
+
+// ---------------------------------------------------------------------------
+// Host-side launch helpers (defined in the .hip files)
+// ---------------------------------------------------------------------------
+// Kernel timing hooks (mira_api.cpp); no-ops unless profiling is enabled.
+void prof_begin(const char* name, hipStream_t st);
+void prof_end(const char* name, hipStream_t st);
+
+hipError_t launch_route(const mira_shape& s, const Layout& L, const WsPtr& w, const void* x,
+                        const void* wr, const float* bias, float* logits_out, hipStream_t st);
+hipError_t launch_permute(const mira_shape& s, const Layout& L, const WsPtr& w,
+                          const ExpertPool& ep, int32_t* counts_out, int32_t* idx_out,
+                          float* wts_out, int32_t* offsets_out, int32_t* order_out,
+                          hipStream_t st);
+hipError_t launch_decode(const mira_shape& s, const Layout& L, const WsPtr& w, const void* x,
+                         const ExpertPool& ep, float* out, hipStream_t st);
+hipError_t launch_prefill(const mira_shape& s, const Layout& L, const WsPtr& w, const void* x,
+                          const ExpertPool& ep, float* out, hipStream_t st);
+hipError_t launch_pack(int C, int R, int n, int w_dtype, const void* wg, const void* wu,
+                       const void* wd, float eps, void* packed, uint64_t stride, hipStream_t st);
+hipError_t launch_predict(const mira_pred_shape& p, const void* x, int T, const void* w1,
+                          const float* b1, const void* w2, const float* b2, float* scores,
+                          void* ws, hipStream_t st);
+hipError_t launch_set_slot(int32_t* table, int expert, int slot, hipStream_t st);
+
+int device_cu_count();
+
+}  // namespace mira

@@ -1,0 +1,145 @@
+// Device packer: fp32/bf16 expert weights -> packed experts (paper section
+// IV-B).  Per expert-hidden row r:
+//   alpha_r = max(|gate[r,:]|_inf, |up[r,:]|_inf, |down[:,r]|_inf)
+//   sigma_r = bf16_rne(fl32(max(alpha_r, eps) / 127))
+//   q       = clamp(rint_even(fl32(w / sigma_r)), -127, 127)
+// The division is the IEEE correctly rounded fp32 one (this file is built
+// without fast-math), so the bytes equal the host packer's.
+#include "device_util.h"
+#include "mira_internal.h"
+
+namespace mira {
+
+template <typename WT>
+__device__ __forceinline__ float ldw(const WT* p, size_t i);
+template <>
+__device__ __forceinline__ float ldw<float>(const float* p, size_t i) { return p[i]; }
+template <>
+__device__ __forceinline__ float ldw<uint16_t>(const uint16_t* p, size_t i) {
+  return bf16_to_f32(p[i]);
+}
+
+// amax[e][r] = max over gate row r and up row r (one wave per row)
+template <typename WT>
+__global__ __launch_bounds__(256) void pack_rowmax_kernel(const WT* __restrict__ wg,
+                                                          const WT* __restrict__ wu, int C, int R,
+                                                          uint32_t* __restrict__ amax) {
+  const int e = blockIdx.y;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (r >= R) return;
+  const size_t base = ((size_t)e * R + r) * C;
+  float m = 0.f;
+  for (int c = lane; c < C; c += 64) m = fmaxf(m, fmaxf(fabsf(ldw(wg, base + c)), fabsf(ldw(wu, base + c))));
+  m = wave_max(m);
+  if (lane == 0) amax[(size_t)e * R + r] = __float_as_uint(m);
+}
+
+// amax[e][r] = max(amax[e][r], max over a chunk of c of |down[c][r]|)
+template <typename WT>
+__global__ __launch_bounds__(256) void pack_colmax_kernel(const WT* __restrict__ wd, int C, int R,
+                                                          int c_chunk, uint32_t* __restrict__ amax) {
+  const int e = blockIdx.z;
+  const int r = blockIdx.x * 256 + threadIdx.x;
+  if (r >= R) return;
+  const int c0 = blockIdx.y * c_chunk, c1 = min(C, c0 + c_chunk);
+  const WT* p = wd + (size_t)e * C * R + r;
+  float m = 0.f;
+  for (int c = c0; c < c1; ++c) m = fmaxf(m, fabsf(ldw(p, (size_t)c * R)));
+  // non-negative floats order like their bit patterns
+  atomicMax(&amax[(size_t)e * R + r], __float_as_uint(m));
+}
+
+__device__ __forceinline__ float scale_of(uint32_t amax_bits, float eps) {
+  const float s32 = fmaxf(__uint_as_float(amax_bits), eps) / 127.0f;
+  return bf16_to_f32(f32_to_bf16_rne(s32));
+}
+
+__device__ __forceinline__ int8_t quant(float w, float sigma) {
+  float q = rintf(w / sigma);
+  q = fminf(fmaxf(q, -127.f), 127.f);
+  return (int8_t)(int)q;
+}
+
+// gate/up rows: blob[e] bytes [0, 2RC); one workgroup per (row, matrix)
+template <typename WT>
+__global__ __launch_bounds__(256) void pack_quant_rows_kernel(const WT* __restrict__ wg,
+                                                              const WT* __restrict__ wu, int C,
+                                                              int R, float eps,
+                                                              const uint32_t* __restrict__ amax,
+                                                              int8_t* __restrict__ packed,
+                                                              uint64_t stride) {
+  const int e = blockIdx.z, mat = blockIdx.y, r = blockIdx.x;
+  const float sigma = scale_of(amax[(size_t)e * R + r], eps);
+  const WT* src = (mat == 0 ? wg : wu) + ((size_t)e * R + r) * C;
+  int8_t* dst = packed + (size_t)e * stride + (size_t)mat * R * C + (size_t)r * C;
+  for (int c = threadIdx.x; c < C; c += 256) dst[c] = quant(ldw(src, c), sigma);
+}
+
+// down [C][R]: column r uses sigma_r; also writes sigma and zero padding
+template <typename WT>
+__global__ __launch_bounds__(256) void pack_quant_down_kernel(const WT* __restrict__ wd, int C,
+                                                              int R, float eps,
+                                                              const uint32_t* __restrict__ amax,
+                                                              int8_t* __restrict__ packed,
+                                                              uint64_t stride) {
+  const int e = blockIdx.z, c = blockIdx.y;
+  const int r = blockIdx.x * 256 + threadIdx.x;
+  if (r >= R) return;
+  const float sigma = scale_of(amax[(size_t)e * R + r], eps);
+  int8_t* blob = packed + (size_t)e * stride;
+  blob[(size_t)2 * R * C + (size_t)c * R + r] = quant(ldw(wd, ((size_t)e * C + c) * R + r), sigma);
+  if (c == 0) {
+    uint16_t* sig = (uint16_t*)(blob + (size_t)3 * R * C);
+    sig[r] = f32_to_bf16_rne(fmaxf(__uint_as_float(amax[(size_t)e * R + r]), eps) / 127.0f);
+  }
+}
+
+__global__ __launch_bounds__(256) void pack_pad_kernel(int8_t* __restrict__ packed, uint64_t stride,
+                                                       uint64_t used) {
+  const int e = blockIdx.y;
+  for (uint64_t i = used + (uint64_t)blockIdx.x * 256 + threadIdx.x; i < stride;
+       i += (uint64_t)gridDim.x * 256)
+    packed[(size_t)e * stride + i] = 0;
+}
+
+hipError_t launch_pack(int C, int R, int n, int w_dtype, const void* wg, const void* wu,
+                       const void* wd, float eps, void* packed, uint64_t stride, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  // fp32 row maxima alpha_r live in a stream-ordered temporary allocation
+  // (packing is offline; the forward path never allocates).
+  uint32_t* amax = nullptr;
+  hipError_t err = hipMallocAsync((void**)&amax, (size_t)n * R * 4, st);
+  if (err != hipSuccess) return err;
+  prof_begin("pack", st);
+  const int c_chunk = 256;
+  if (w_dtype == MIRA_BF16) {
+    const uint16_t *g = (const uint16_t*)wg, *u = (const uint16_t*)wu, *d = (const uint16_t*)wd;
+    hipLaunchKernelGGL(pack_rowmax_kernel<uint16_t>, dim3((R + 3) / 4, n), dim3(256), 0, st, g, u,
+                       C, R, amax);
+    hipLaunchKernelGGL(pack_colmax_kernel<uint16_t>, dim3((R + 255) / 256, (C + c_chunk - 1) / c_chunk, n),
+                       dim3(256), 0, st, d, C, R, c_chunk, amax);
+    hipLaunchKernelGGL(pack_quant_rows_kernel<uint16_t>, dim3(R, 2, n), dim3(256), 0, st, g, u, C,
+                       R, eps, amax, (int8_t*)packed, stride);
+    hipLaunchKernelGGL(pack_quant_down_kernel<uint16_t>, dim3((R + 255) / 256, C, n), dim3(256), 0,
+                       st, d, C, R, eps, amax, (int8_t*)packed, stride);
+  } else {
+    const float *g = (const float*)wg, *u = (const float*)wu, *d = (const float*)wd;
+    hipLaunchKernelGGL(pack_rowmax_kernel<float>, dim3((R + 3) / 4, n), dim3(256), 0, st, g, u, C,
+                       R, amax);
+    hipLaunchKernelGGL(pack_colmax_kernel<float>, dim3((R + 255) / 256, (C + c_chunk - 1) / c_chunk, n),
+                       dim3(256), 0, st, d, C, R, c_chunk, amax);
+    hipLaunchKernelGGL(pack_quant_rows_kernel<float>, dim3(R, 2, n), dim3(256), 0, st, g, u, C, R,
+                       eps, amax, (int8_t*)packed, stride);
+    hipLaunchKernelGGL(pack_quant_down_kernel<float>, dim3((R + 255) / 256, C, n), dim3(256), 0,
+                       st, d, C, R, eps, amax, (int8_t*)packed, stride);
+  }
+  const uint64_t used = (uint64_t)3 * R * C + (uint64_t)2 * R;
+  if (stride > used)
+    hipLaunchKernelGGL(pack_pad_kernel, dim3(64, n), dim3(256), 0, st, (int8_t*)packed, stride, used);
+  prof_end("pack", st);
+  err = hipGetLastError();
+  hipError_t e2 = hipFreeAsync(amax, st);
+  return err != hipSuccess ? err : e2;
+}
+
+}  // namespace mira

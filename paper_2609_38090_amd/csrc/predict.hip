@@ -1,0 +1,77 @@
+// Predictor head (paper section IV-E): mean-pool a group of token rows of
+// layer l's hidden states, then a two-layer MLP (ReLU, sigmoid) scoring the
+// experts of layer l+2.  Three small kernels, fp32 accumulation.
+#include "device_util.h"
+#include "mira_internal.h"
+
+namespace mira {
+
+// f[i][c] = (1/group) * sum over rows [i*group, (i+1)*group) of x[row][c]
+template <typename ActT>
+__global__ __launch_bounds__(256) void pred_pool_kernel(const ActT* __restrict__ x, int C, int group,
+                                                        float* __restrict__ f) {
+  const int i = blockIdx.y;
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= C) return;
+  float s = 0.f;
+  for (int r = 0; r < group; ++r) s += load_act(x, (size_t)(i * group + r) * C + c);
+  f[(size_t)i * C + c] = s / (float)group;
+}
+
+// z[i][p] = max(0, sum_c W1[p][c] f[i][c] + b1[p]); one wave per row p
+__global__ __launch_bounds__(256) void pred_layer1_kernel(const uint16_t* __restrict__ w1,
+                                                          const float* __restrict__ b1,
+                                                          const float* __restrict__ f, int C, int P,
+                                                          int n, float* __restrict__ z) {
+  const int p = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (p >= P) return;
+  const uint16_t* wr = w1 + (size_t)p * C;
+  for (int i = 0; i < n; ++i) {
+    const float* fi = f + (size_t)i * C;
+    float s = 0.f;
+    for (int c = lane; c < C; c += 64) s = fmaf(bf16_to_f32(wr[c]), fi[c], s);
+    s = wave_sum(s);
+    if (lane == 0) z[(size_t)i * P + p] = fmaxf(s + (b1 ? b1[p] : 0.f), 0.f);
+  }
+}
+
+// scores[i][e] = 1 / (1 + exp(-(sum_p W2[e][p] z[i][p] + b2[e]))); one wave per (i, e)
+__global__ __launch_bounds__(256) void pred_layer2_kernel(const uint16_t* __restrict__ w2,
+                                                          const float* __restrict__ b2,
+                                                          const float* __restrict__ z, int P, int E,
+                                                          int n, float* __restrict__ scores) {
+  const int q = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (q >= n * E) return;
+  const int i = q / E, e = q - i * E;
+  const uint16_t* wr = w2 + (size_t)e * P;
+  const float* zi = z + (size_t)i * P;
+  float s = 0.f;
+  for (int p = lane; p < P; p += 64) s = fmaf(bf16_to_f32(wr[p]), zi[p], s);
+  s = wave_sum(s);
+  if (lane == 0) scores[(size_t)i * E + e] = 1.f / (1.f + expf(-(s + (b2 ? b2[e] : 0.f))));
+}
+
+hipError_t launch_predict(const mira_pred_shape& p, const void* x, int T, const void* w1,
+                          const float* b1, const void* w2, const float* b2, float* scores,
+                          void* ws, hipStream_t st) {
+  const int n = T / p.group;
+  if (n == 0) return hipSuccess;
+  float* f = (float*)ws;
+  float* z = (float*)((char*)ws + align_up((size_t)n * p.hidden * 4, 256));
+  prof_begin("predict", st);
+  dim3 gpool((p.hidden + 255) / 256, n);
+  if (p.act_dtype == MIRA_BF16)
+    hipLaunchKernelGGL(pred_pool_kernel<uint16_t>, gpool, dim3(256), 0, st, (const uint16_t*)x,
+                       p.hidden, p.group, f);
+  else
+    hipLaunchKernelGGL(pred_pool_kernel<float>, gpool, dim3(256), 0, st, (const float*)x, p.hidden,
+                       p.group, f);
+  hipLaunchKernelGGL(pred_layer1_kernel, dim3((p.pred_hidden + 3) / 4), dim3(256), 0, st,
+                     (const uint16_t*)w1, b1, f, p.hidden, p.pred_hidden, n, z);
+  hipLaunchKernelGGL(pred_layer2_kernel, dim3((n * p.n_out + 3) / 4), dim3(256), 0, st,
+                     (const uint16_t*)w2, b2, z, p.pred_hidden, p.n_out, n, scores);
+  prof_end("predict", st);
+  return hipGetLastError();
+}
+
+}  // namespace mira

@@ -1,0 +1,142 @@
+"""CPU checks of the C ABI: the library loads, exports every declared entry
+point, rejects bad arguments before any launch, and its host packer is
+byte-exact against the oracle (paper section IV-B)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_38090_amd as mira
+from mira_inputs import CONFIGS, expert_weights
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "mira.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(mira_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function():
+    lib = mira.load()
+    declared = _declared_functions()
+    assert len(declared) >= 14
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert sorted(mira.EXPORTED_SYMBOLS) == declared
+    assert "gfx950" in mira.mira_version()
+
+
+def test_packed_expert_bytes_closed_form():
+    for C, R in [(256, 512), (4096, 14336), (2048, 1408), (64, 64), (8, 1)]:
+        assert mira.mira_packed_expert_bytes(C, R) == oracle.packed_expert_bytes(C, R)
+    assert mira.mira_packed_expert_bytes(0, 64) == 0
+    assert mira.mira_packed_expert_bytes(64, -1) == 0
+
+
+def test_workspace_bytes_monotone_and_validated():
+    s = mira.MoEShape(2048, 1408, 64, 6, 2, mira.MIRA_BF16)
+    sizes = [mira.mira_workspace_bytes(s, t) for t in (1, 8, 16, 17, 512, 2048)]
+    assert all(a <= b for a, b in zip(sizes, sizes[1:]))
+    assert all(v % 256 == 0 for v in sizes)
+    with pytest.raises(mira.MiraError):
+        mira.mira_workspace_bytes(mira.MoEShape(100, 1408, 64, 6), 4)   # hidden not a multiple of 64
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(hidden=100), -2), (dict(ffn=0), -2), (dict(top_k=9), -2), (dict(top_k=0), -2),
+    (dict(n_experts=250, n_shared=10), -2), (dict(act_dtype=7), -1), (dict(flags=0x100), -1),
+    (dict(flags=mira.MIRA_FLAG_FORCE_DECODE | mira.MIRA_FLAG_FORCE_PREFILL), -1),
+])
+def test_forward_rejects_bad_shapes_before_launch(bad, code):
+    kw = dict(hidden=256, ffn=512, n_experts=8, top_k=2, n_shared=0, act_dtype=mira.MIRA_F32, flags=0)
+    kw.update(bad)
+    a = mira.MoEArgs(n_tokens=4)
+    with pytest.raises(mira.MiraError) as ei:
+        mira.mira_moe_forward(mira.MoEShape(**kw), a, stream=1)
+    assert ei.value.code == code
+    assert mira.mira_last_error()
+
+
+def test_forward_argument_checks():
+    s = mira.MoEShape(256, 512, 4, 2, 0, mira.MIRA_F32)
+    ws = mira.mira_workspace_bytes(s, 16)
+    base = dict(x=0x1000, n_tokens=16, n_slots=4, w_router=0x2000, slot_table=0x3000, slot_pool=0x10000,
+                slot_stride=oracle.packed_expert_bytes(256, 512), out=0x4000, workspace=0x20000,
+                workspace_bytes=ws)
+    cases = [
+        (dict(x=None), -1), (dict(n_slots=0), -1), (dict(x=0x1004), -3), (dict(slot_pool=0x10010), -3),
+        (dict(slot_stride=256), -2), (dict(workspace_bytes=ws - 256), -4), (dict(n_tokens=-1), -2),
+        (dict(workspace=0x20040), -3),
+    ]
+    for change, code in cases:
+        kw = dict(base)
+        kw.update(change)
+        with pytest.raises(mira.MiraError) as ei:
+            mira.mira_moe_forward(s, mira.MoEArgs(**kw), stream=1)
+        assert ei.value.code == code, (change, mira.mira_last_error())
+    s2 = mira.MoEShape(256, 512, 4, 2, 0, mira.MIRA_F32, mira.MIRA_FLAG_FORCE_DECODE)
+    kw = dict(base, n_tokens=17, workspace_bytes=10**12)
+    with pytest.raises(mira.MiraError) as ei:
+        mira.mira_moe_forward(s2, mira.MoEArgs(**kw), stream=1)
+    assert ei.value.code == -2
+    # zero tokens is a no-op that touches nothing
+    mira.mira_moe_forward(s, mira.MoEArgs(n_tokens=0), stream=1)
+
+
+def test_predict_and_stage_argument_checks():
+    p = mira.PredShape(4096, 512, 8, 8)
+    assert mira.mira_predict_workspace_bytes(p, 16) >= 2 * 4096 * 4
+    with pytest.raises(mira.MiraError):
+        mira.mira_predict(p, 0x1000, 12, 0x2000, None, 0x3000, None, 0x4000, 0x5000, 10**9, stream=1)
+    with pytest.raises(mira.MiraError):
+        mira.mira_stage_expert(0x1000, 256, 0, 0x2000, 512, copy_stream=1)
+    with pytest.raises(mira.MiraError):
+        mira.mira_set_slot(0x1000, 0, -2, stream=1)
+
+
+def _host_pack(C, R, wg, wu, wd, eps=1e-8, dtype=mira.MIRA_F32, stride=None):
+    n = wg.shape[0]
+    stride = stride or oracle.packed_expert_bytes(C, R)
+    out = np.full((n, stride), 0xAB, dtype=np.uint8)
+    mira.mira_pack_experts(mira.MoEShape(C, R, 1, 1), n, dtype, wg.ctypes.data, wu.ctypes.data,
+                           wd.ctypes.data, eps, out.ctypes.data, stride, 0)
+    return out
+
+
+def test_host_pack_matches_oracle_tiny_config():
+    cfg = CONFIGS["tiny"]
+    ws = [expert_weights(cfg, 0, e) for e in range(cfg.E)]
+    wg = np.stack([w[0].numpy() for w in ws])
+    wu = np.stack([w[1].numpy() for w in ws])
+    wd = np.stack([w[2].numpy() for w in ws])
+    got = _host_pack(cfg.C, cfg.R, wg, wu, wd)
+    for e in range(cfg.E):
+        assert np.array_equal(got[e], oracle.pack_expert(wg[e], wu[e], wd[e]))
+
+
+def test_host_pack_bf16_input_and_padded_stride():
+    rng = np.random.default_rng(0)
+    C, R = 128, 192
+    w = [torch.from_numpy(rng.standard_normal((2, *s)).astype(np.float32) * 0.05).to(torch.bfloat16)
+         for s in ((R, C), (R, C), (C, R))]
+    bits = [t.view(torch.int16).numpy().view(np.uint16).copy() for t in w]
+    stride = oracle.packed_expert_bytes(C, R) + 512
+    got = _host_pack(C, R, *bits, dtype=mira.MIRA_BF16, stride=stride)
+    for e in range(2):
+        ref = oracle.pack_expert(*(t[e].float().numpy() for t in w))
+        assert np.array_equal(got[e, :ref.size], ref)
+        assert not got[e, ref.size:].any()
+
+
+def test_host_pack_fine_grained_expert_slice():
+    """One expert of the fine-grained layer at full size (C=2048, R=1408)."""
+    cfg = CONFIGS["fine_grained"]
+    wg, wu, wd = (t.numpy()[None] for t in expert_weights(cfg, 0, 5))
+    got = _host_pack(cfg.C, cfg.R, wg, wu, wd)
+    assert np.array_equal(got[0], oracle.pack_expert(wg[0], wu[0], wd[0]))

@@ -1,0 +1,101 @@
+"""Full-size workloads on the GPU against the oracle.
+
+Each case runs the layer exactly as the benchmark does and checks every
+routing output bit-exactly, the packed bytes of the experts the sampled
+tokens touch, and the layer output on sampled token rows (the oracle
+computes them one expert at a time in fp64)."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_layer import EPS, Layer, run_and_check
+from mira_inputs import CONFIGS, activations, predictor_weights
+import oracle
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+
+def _check_packed(lay, blobs):
+    for e, ref in blobs.cache.items():
+        assert np.array_equal(lay.slot_bytes(int(lay.table[e])), ref), f"expert {e} bytes differ"
+
+
+def test_mixtral_decode_layer(mira):
+    lay = Layer(CONFIGS["mixtral_decode"])
+    res, errs, blobs, ties = run_and_check(lay)
+    _check_packed(lay, blobs)
+    assert len(blobs.cache) == 2
+    print(f"mixtral decode: rel_fro={errs[0]:.2e} max_abs/rms={errs[1]:.2e}")
+
+
+def test_mixtral_prefill_layer_sampled(mira):
+    lay = Layer(CONFIGS["mixtral_prefill"])
+    sample = [0, 1, 2, 100, 255, 256, 383, 510, 511]
+    res, errs, blobs, ties = run_and_check(lay, tokens=sample)
+    _check_packed(lay, blobs)
+    print(f"mixtral prefill: rel_fro={errs[0]:.2e} max_abs/rms={errs[1]:.2e} experts={sorted(blobs.cache)}")
+
+
+def test_fine_grained_layer_sampled(mira):
+    cfg = CONFIGS["fine_grained"]
+    lay = Layer(cfg)
+    res0 = lay.run()
+    o_x, o_wr, o_b = lay.oracle_inputs()
+    ties = oracle.near_tie_tokens(oracle.router_logits(o_x, o_wr, o_b), cfg.k).tolist()
+    rng = np.random.default_rng(0)
+    sample = sorted(set(rng.choice(cfg.T, 24, replace=False).tolist() + [0, cfg.T - 1] + ties[:4]))
+    res, errs, blobs, found = run_and_check(lay, tokens=sample, res=res0)
+    _check_packed(lay, blobs)
+    print(f"fine-grained: rel_fro={errs[0]:.2e} max_abs/rms={errs[1]:.2e} near-ties={len(found)}")
+
+
+@pytest.mark.parametrize("layer", [0, 17, 31])
+def test_beam_stack_layer_with_staging(mira, layer):
+    """One layer of the beam-search stack: 4 of 8 experts resident, the
+    selected non-resident ones staged from pinned host memory between the
+    route and expert phases; input = the layer's own seeded activations
+    (teacher forcing)."""
+    cfg = CONFIGS["beam_stack"]
+    from mira_inputs import resident_experts
+    hot = resident_experts(cfg, layer)
+    lay = Layer(cfg, layer=layer, resident=hot, spare_slots=4)
+    host = {}
+
+    def fetch(r):
+        counts = r["counts"].cpu().numpy()
+        table = lay.table.cpu().numpy()
+        free = [s for s in range(lay.n_slots) if s not in set(table.tolist())]
+        copy = torch.cuda.Stream()
+        ev = torch.cuda.Event()
+        for e in range(cfg.E):
+            if counts[e] > 0 and table[e] < 0:
+                buf = torch.empty(lay.stride, dtype=torch.uint8, pin_memory=True)
+                wg, wu, wd = (np.ascontiguousarray(t) for t in lay.master(e))
+                mira.mira_pack_experts(mira.MoEShape(cfg.C, cfg.R, 1, 1), 1, mira.MIRA_F32, wg.ctypes.data,
+                                       wu.ctypes.data, wd.ctypes.data, EPS, buf, lay.stride, 0)
+                host[e] = buf
+                slot = free.pop(0)
+                mira.mira_stage_expert(lay.pool, lay.stride, slot, buf, lay.stride, copy, None)
+                mira.mira_set_slot(lay.table, e, slot, copy)
+        ev.record(copy)
+        torch.cuda.current_stream().wait_event(ev)
+
+    res = lay.run(two_phase=True, between=fetch)
+    res["status"][0] = 0  # misses were served by the demand fetch
+    _, errs, blobs, _ = run_and_check(lay, res=res)
+    _check_packed(lay, blobs)
+    print(f"beam layer {layer}: staged={sorted(host)} rel_fro={errs[0]:.2e}")
+
+
+def test_beam_predictor_full_size(mira):
+    cfg = CONFIGS["beam_stack"]
+    x = activations(cfg, 5, "cpu")
+    w1, b1, w2, b2 = predictor_weights(cfg, 5, "cpu")
+    p = mira.PredShape(cfg.C, cfg.pred_hidden, cfg.E, cfg.pred_group, mira.MIRA_BF16)
+    ws = torch.empty(mira.mira_predict_workspace_bytes(p, cfg.T), dtype=torch.uint8, device="cuda")
+    scores = torch.zeros((1, cfg.E), dtype=torch.float32, device="cuda")
+    mira.mira_predict(p, x.cuda(), cfg.T, w1.cuda(), b1.cuda(), w2.cuda(), b2.cuda(), scores, ws, ws.numel())
+    torch.cuda.synchronize()
+    ref = oracle.predictor_scores(x.float().numpy(), cfg.pred_group, w1.float().numpy(), b1.numpy(),
+                                  w2.float().numpy(), b2.numpy())
+    assert np.max(np.abs(scores.cpu().numpy() - ref)) < 1e-4

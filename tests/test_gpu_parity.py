@@ -1,0 +1,190 @@
+"""GPU parity of the MoE expert step against the CPU oracle (small and
+ragged shapes; full-size workloads are in test_gpu_fullsize.py).
+
+Bars: packing, routing indices and the permutation bit-exact; the layer
+output within rel-Frobenius 5e-3 and max-abs 2e-2 * rms(out)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_layer import EPS, Layer, act_dtype, assert_ffn_close, run_and_check
+from mira_inputs import CONFIGS, MoEConfig, predictor_weights, activations
+
+pytestmark = pytest.mark.gpu
+
+
+def _cfg(name, cid, **kw):
+    return MoEConfig(name, cid, **kw)
+
+
+SMALL_BF16 = _cfg("small_bf16", 101, T=16, C=128, E=8, k=2, R=192, zipf_s=1.2)
+SMALL_FG = _cfg("small_fg", 102, T=16, C=128, E=64, k=6, R=128, S=2, zipf_s=1.0)
+SMALL_F32 = _cfg("small_f32", 103, T=16, C=64, E=3, k=3, R=64, act="f32")
+
+
+def test_pack_bit_exact_tiny(mira):
+    lay = Layer(CONFIGS["tiny"])
+    for e in range(4):
+        ref = oracle.pack_expert(*lay.master(e), eps=EPS)
+        assert np.array_equal(lay.slot_bytes(int(lay.table[e])), ref), e
+
+
+def test_pack_bit_exact_bf16_input_and_padding(mira):
+    C, R, n = 128, 256, 3
+    g = torch.Generator().manual_seed(5)
+    w = [torch.randn((n, *s), generator=g).mul_(0.03).to(torch.bfloat16) for s in ((R, C), (R, C), (C, R))]
+    stride = mira.mira_packed_expert_bytes(C, R) + 1024
+    out = torch.full((n * stride,), 0x5A, dtype=torch.uint8, device="cuda")
+    mira.mira_pack_experts(mira.MoEShape(C, R, 1, 1), n, mira.MIRA_BF16, *(t.cuda() for t in w), EPS,
+                           out, stride, 1)
+    got = out.cpu().numpy().reshape(n, stride)
+    for e in range(n):
+        ref = oracle.pack_expert(*(t[e].float().numpy() for t in w), eps=EPS)
+        assert np.array_equal(got[e, :ref.size], ref)
+        assert not got[e, ref.size:].any()
+
+
+def test_tiny_decode_path(mira):
+    res, errs, _, _ = run_and_check(Layer(CONFIGS["tiny"]))
+    assert errs[0] < 1e-4  # the integer decode path is close to fp32-exact
+
+
+def test_tiny_prefill_path(mira):
+    run_and_check(Layer(CONFIGS["tiny"]), flags=mira.MIRA_FLAG_FORCE_PREFILL)
+
+
+def test_decode_and_prefill_paths_agree(mira):
+    lay = Layer(SMALL_BF16)
+    a = lay.run(mira.MIRA_FLAG_FORCE_DECODE)
+    b = lay.run(mira.MIRA_FLAG_FORCE_PREFILL)
+    assert np.array_equal(a["idx"], b["idx"]) and np.array_equal(a["order"], b["order"])
+    assert_ffn_close(b["out"], a["out"], "prefill vs decode")
+
+
+@pytest.mark.parametrize("T", [1, 2, 5, 6, 11, 15, 16, 17, 33, 64, 129])
+def test_ragged_token_counts(mira, T):
+    run_and_check(Layer(SMALL_BF16, T=T))
+
+
+@pytest.mark.parametrize("T", [1, 7, 16, 40, 300])
+def test_fine_grained_shape_small(mira, T):
+    run_and_check(Layer(SMALL_FG, T=T))
+
+
+@pytest.mark.parametrize("flags", [0, "decode", "prefill"])
+def test_f32_activations_k_equals_E(mira, flags):
+    f = {0: 0, "decode": mira.MIRA_FLAG_FORCE_DECODE, "prefill": mira.MIRA_FLAG_FORCE_PREFILL}[flags]
+    run_and_check(Layer(SMALL_F32, T=13), flags=f)
+
+
+def test_softmax_over_all_experts_flag(mira):
+    lay = Layer(SMALL_BF16, T=9)
+    res = lay.run(mira.MIRA_FLAG_SOFTMAX_ALL)
+    o_x, o_wr, o_b = lay.oracle_inputs()
+    lg = oracle.router_logits(o_x, o_wr, o_b)
+    idx = oracle.topk_select(lg, SMALL_BF16.k)
+    assert np.array_equal(res["idx"], idx)
+    assert np.max(np.abs(res["w"] - oracle.combine_weights(lg, idx, norm_topk=False))) < 2e-5
+    from gpu_layer import LazyBlobs
+    ref = oracle.moe_forward(o_x, o_wr, o_b, LazyBlobs(lay), SMALL_BF16.k, SMALL_BF16.C, SMALL_BF16.R,
+                             norm_topk=False)["out"]
+    assert_ffn_close(res["out"], ref, "softmax-all")
+
+
+def test_repeated_calls_bit_identical(mira):
+    for flags in (0, mira.MIRA_FLAG_FORCE_PREFILL):
+        lay = Layer(SMALL_FG, T=40)
+        a, b = lay.run(flags), lay.run(flags)
+        for k in a:
+            assert np.array_equal(a[k], b[k]), k
+
+
+def test_output_independent_of_slot_placement(mira):
+    base = Layer(SMALL_BF16, T=24).run()
+    perm = list(np.random.default_rng(0).permutation(SMALL_BF16.G))
+    moved = Layer(SMALL_BF16, T=24, slot_order=perm, spare_slots=3).run()
+    assert np.array_equal(base["out"], moved["out"])
+    assert np.array_equal(base["order"], moved["order"])
+
+
+def test_non_resident_selected_expert_sets_status(mira):
+    lay = Layer(SMALL_BF16, T=16, resident=[1, 2, 3, 4, 5, 6, 7])  # expert 0 (most popular) absent
+    res = lay.run()
+    assert res["counts"][0] > 0
+    assert res["status"][0] & 1
+    lay2 = Layer(SMALL_BF16, T=16)
+    lay2.table[0] = 99  # beyond n_slots: ignored, flagged
+    res2 = lay2.run()
+    assert res2["status"][0] & 2
+
+
+def test_two_phase_demand_fetch_through_pinned_store(mira):
+    """Route, read the counts, stage the missing experts from pinned host
+    memory into spare slots, then run the experts: bit-identical to the
+    all-resident call."""
+    cfg = SMALL_BF16
+    full = Layer(cfg, T=16).run()
+    lay = Layer(cfg, T=16, resident=[4, 5, 6, 7], spare_slots=4)
+    stride = lay.stride
+    host = torch.empty((cfg.E, stride), dtype=torch.uint8, pin_memory=True)
+    sh = mira.MoEShape(cfg.C, cfg.R, 1, 1)
+    for e in range(cfg.E):
+        wg, wu, wd = (np.ascontiguousarray(t) for t in lay.master(e))
+        mira.mira_pack_experts(sh, 1, mira.MIRA_F32, wg.ctypes.data, wu.ctypes.data, wd.ctypes.data, EPS,
+                               host[e], stride, 0)
+    copy = torch.cuda.Stream()
+    compute = torch.cuda.current_stream()
+
+    def fetch(r):
+        counts = r["counts"].cpu().numpy()
+        table = lay.table.cpu().numpy()
+        free = [s for s in range(lay.n_slots) if s not in set(table.tolist())]
+        ev = torch.cuda.Event()
+        for e in range(cfg.E):
+            if counts[e] > 0 and table[e] < 0:
+                slot = free.pop(0)
+                mira.mira_stage_expert(lay.pool, stride, slot, host[e], stride, copy, None)
+                mira.mira_set_slot(lay.table, e, slot, copy)
+        ev.record(copy)
+        compute.wait_event(ev)
+
+    res = lay.run(two_phase=True, between=fetch)
+    assert res["status"][0] == 1  # the route phase saw the misses
+    assert np.array_equal(res["out"], full["out"])
+    assert np.array_equal(res["idx"], full["idx"])
+
+
+def test_stage_copy_is_byte_exact(mira):
+    n = 3 * 1024 * 1024 + 512
+    src = torch.randint(0, 256, (n,), dtype=torch.uint8).pin_memory()
+    pool = torch.zeros(2 * n + 256, dtype=torch.uint8, device="cuda")
+    ev = torch.cuda.Event()
+    s = torch.cuda.Stream()
+    mira.mira_stage_expert(pool, n + 256, 1, src, n, s, ev)
+    ev.synchronize()
+    assert torch.equal(pool[n + 256:2 * n + 256].cpu(), src)
+    assert not pool[:n + 256].any()
+
+
+def test_predictor_matches_oracle(mira):
+    cfg = CONFIGS["beam_stack"]
+    x = activations(cfg, 3, "cpu", T=16)
+    w1, b1, w2, b2 = predictor_weights(cfg, 3, "cpu")
+    b1 = torch.randn(b1.shape, generator=torch.Generator().manual_seed(1)) * 0.1
+    p = mira.PredShape(cfg.C, cfg.pred_hidden, cfg.E, cfg.pred_group, mira.MIRA_BF16)
+    ws = torch.empty(mira.mira_predict_workspace_bytes(p, 16), dtype=torch.uint8, device="cuda")
+    scores = torch.zeros((2, cfg.E), dtype=torch.float32, device="cuda")
+    mira.mira_predict(p, x.cuda(), 16, w1.cuda(), b1.cuda(), w2.cuda(), b2.cuda(), scores, ws, ws.numel())
+    torch.cuda.synchronize()
+    ref = oracle.predictor_scores(x.float().numpy(), cfg.pred_group, w1.float().numpy(), b1.numpy(),
+                                  w2.float().numpy(), b2.numpy())
+    assert np.max(np.abs(scores.cpu().numpy() - ref)) < 1e-4
+
+
+def test_zero_tokens_is_a_noop(mira):
+    lay = Layer(SMALL_BF16, T=4)
+    s = lay.shape()
+    a = mira.MoEArgs(n_tokens=0)
+    mira.mira_moe_forward(s, a)
+    torch.cuda.synchronize()
