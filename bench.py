@@ -1,0 +1,279 @@
+"""Benchmark of the Mira MoE expert step on one MI355X.
+
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+A step is one MoE layer call (router, top-k, permutation, expert FFN over
+packed experts, combine) on one batch of the workload; the beam workload's
+step also runs the predictor head.  Inputs are seeded synthetic tensors of
+the workload's shapes, resident in HBM before timing starts.  Weights are
+rotated over several packed copies of the layer so every call streams cold
+expert bytes (more than 1 GB between reuses, above the 256 MB Infinity Cache).
+
+Prints one JSON line with the throughput (tokens/s), the roofline of the
+dominant kernel (timed with HIP events on its stream inside the timed
+region) and the CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "MoE-layer tokens/s (decode+prefill); HBM GB/s on packed experts vs peak"
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+COLD_BYTES = 1 << 30
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--workload", default="mixtral_decode",
+                   choices=["tiny", "mixtral_decode", "mixtral_prefill", "fine_grained", "beam_stack"])
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-profile", action="store_true", help="skip the per-kernel HIP-event timing")
+    p.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample")
+    return p.parse_args()
+
+
+def build_copies(cfg, n_copies):
+    """n_copies packed copies of the layer (different seeded weights per copy)."""
+    import torch
+    import paper_2609_38090_amd as mira
+    from mira_inputs import activations, expert_weights, router_bias, router_weights
+
+    stride = mira.mira_packed_expert_bytes(cfg.C, cfg.R)
+    act = mira.MIRA_F32 if cfg.act == "f32" else mira.MIRA_BF16
+    pack_shape = mira.MoEShape(cfg.C, cfg.R, 1, 1)
+    copies = []
+    for l in range(n_copies):
+        pool = torch.empty(cfg.G * stride, dtype=torch.uint8, device="cuda")
+        for e in range(cfg.G):
+            wg, wu, wd = expert_weights(cfg, l, e, "cuda")
+            mira.mira_pack_experts(pack_shape, 1, mira.MIRA_F32, wg, wu, wd, 1e-8,
+                                   pool[e * stride:], stride, 1)
+            del wg, wu, wd
+        b = router_bias(cfg, l)
+        copies.append(dict(
+            pool=pool,
+            table=torch.arange(cfg.G, dtype=torch.int32, device="cuda"),
+            x=activations(cfg, l, "cuda"),
+            wr=router_weights(cfg, l, "cuda"),
+            bias=None if b is None else b.cuda(),
+        ))
+    torch.cuda.synchronize()
+    return copies, stride, act
+
+
+def algorithmic_units(cfg, counts):
+    """Packed-expert bytes and FLOPs one call must touch, from the routed counts."""
+    active = [g for g in range(cfg.G) if counts[g] > 0]
+    pairs = int(sum(counts))
+    gu_bytes = len(active) * (2 * cfg.R * cfg.C + 2 * cfg.R)
+    dn_bytes = len(active) * (cfg.C * cfg.R)
+    gu_flops = pairs * 4.0 * cfg.C * cfg.R
+    dn_flops = pairs * 2.0 * cfg.C * cfg.R
+    return dict(active=len(active), pairs=pairs, gu_bytes=gu_bytes, dn_bytes=dn_bytes,
+                gu_flops=gu_flops, dn_flops=dn_flops)
+
+
+def cpu_baseline(cfg, copy0, budget_s):
+    """The oracle, as it stands, on a bounded sample of the same workload."""
+    import numpy as np
+    import oracle
+    from mira_inputs import expert_weights
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        blas_threads = 1
+    x = copy0["x"].float().cpu().numpy().astype(np.float64)
+    wr = copy0["wr"].float().cpu().numpy().astype(np.float64)
+    b = None if copy0["bias"] is None else copy0["bias"].cpu().numpy().astype(np.float64)
+    logits = oracle.router_logits(x, wr, b)
+    idx = oracle.topk_select(logits, cfg.k)
+    # pack the experts the sample needs (offline step, timed separately)
+    t0 = time.perf_counter()
+    blobs = {}
+    tokens = []
+    deadline = time.perf_counter() + budget_s
+    for t in range(cfg.T):
+        need = [int(e) for e in idx[t] if int(e) not in blobs]
+        for e in need:
+            wg, wu, wd = (w.cpu().numpy() for w in expert_weights(cfg, 0, e, "cuda"))
+            blobs[e] = oracle.pack_expert(wg, wu, wd)
+        tokens.append(t)
+        if time.perf_counter() > deadline or len(tokens) >= 64:
+            break
+    shared = [oracle.pack_expert(*(w.cpu().numpy() for w in expert_weights(cfg, 0, cfg.E + s, "cuda")))
+              for s in range(cfg.S)]
+    pack_s = time.perf_counter() - t0
+
+    class Blobs:
+        def __len__(self):
+            return cfg.E
+
+        def __getitem__(self, e):
+            return blobs[e]
+
+    t1 = time.perf_counter()
+    oracle.moe_forward(x, wr, b, Blobs(), cfg.k, cfg.C, cfg.R, shared_blobs=shared, tokens=tokens)
+    fwd_s = time.perf_counter() - t1
+    return {
+        "value": round(len(tokens) / fwd_s, 4),
+        "unit": "tokens/s",
+        "cores": int(blas_threads),
+        "kind": "oracle",
+        "sample": (f"numpy fp64 oracle forward (router, top-k, expert FFN one expert at a time, combine) "
+                   f"on the first {len(tokens)} token(s) of layer copy 0 of the same workload; "
+                   f"{len(blobs) + len(shared)} experts packed beforehand in {pack_s:.1f} s (not timed); "
+                   f"forward took {fwd_s:.2f} s; BLAS threads {blas_threads}, "
+                   f"host CPUs available {len(os.sched_getaffinity(0))}"),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        print("bench.py measures the single-GPU MoE expert step; multi-GPU runs are not part "
+              "of this build (see the sharding notes in DESIGN.md).", file=sys.stderr)
+        return 2
+
+    import torch
+    import paper_2609_38090_amd as mira
+    from mira_inputs import CONFIGS
+
+    mira.load()
+    cfg = CONFIGS[args.workload]
+    # bytes of packed experts one call can touch: at most min(G, T*k + S) experts
+    touched = min(cfg.G, cfg.T * cfg.k + cfg.S) * mira.mira_packed_expert_bytes(cfg.C, cfg.R)
+    n_copies = max(2, min(8, math.ceil(COLD_BYTES / max(1, touched)) + 1))
+    if cfg.name == "tiny":
+        n_copies = 1
+    copies, stride, act = build_copies(cfg, n_copies)
+    shape = mira.MoEShape(cfg.C, cfg.R, cfg.E, cfg.k, cfg.S, act, 0)
+    T = cfg.T
+    ws = torch.empty(mira.mira_workspace_bytes(shape, T), dtype=torch.uint8, device="cuda")
+    out = torch.empty((T, cfg.C), dtype=torch.float32, device="cuda")
+    counts = torch.zeros((cfg.G,), dtype=torch.int32, device="cuda")
+    argsets = []
+    for c in copies:
+        argsets.append(mira.MoEArgs(x=c["x"], n_tokens=T, n_slots=cfg.G, w_router=c["wr"],
+                                    router_bias=c["bias"], slot_table=c["table"], slot_pool=c["pool"],
+                                    slot_stride=stride, out=out, expert_counts=counts, workspace=ws,
+                                    workspace_bytes=ws.numel()))
+    pred = None
+    if cfg.pred_hidden:
+        from mira_inputs import predictor_weights
+        w1, b1, w2, b2 = (t.cuda() for t in predictor_weights(cfg, 0, "cpu"))
+        ps = mira.PredShape(cfg.C, cfg.pred_hidden, cfg.E, cfg.pred_group, act)
+        pws = torch.empty(mira.mira_predict_workspace_bytes(ps, T), dtype=torch.uint8, device="cuda")
+        scores = torch.empty((T // cfg.pred_group, cfg.E), dtype=torch.float32, device="cuda")
+        pred = (ps, w1, b1, w2, b2, scores, pws)
+
+    stream = torch.cuda.current_stream()
+
+    def step(i):
+        a = argsets[i % len(argsets)]
+        mira.mira_moe_forward(shape, a, stream)
+        if pred is not None:
+            ps, w1, b1, w2, b2, scores, pws = pred
+            mira.mira_predict(ps, a.x, T, w1, b1, w2, b2, scores, pws, pws.numel(), stream)
+
+    # routed counts of each copy (for the algorithmic byte / flop counts)
+    units = []
+    for i in range(len(argsets)):
+        step(i)
+        torch.cuda.synchronize()
+        units.append(algorithmic_units(cfg, counts.cpu().tolist()))
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    decode = T <= mira.MIRA_DECODE_MAX_TOKENS
+    dominant = "decode_gateup" if decode else "prefill_gateup"
+    if not args.no_profile:
+        # only the dominant kernel carries event records (events cost time)
+        mira.mira_profile_select(dominant)
+        mira.mira_profile_enable(True)
+        mira.mira_profile_read()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    prof = {}
+    if not args.no_profile:
+        prof = mira.mira_profile_read()
+        mira.mira_profile_enable(False)
+
+    ms = elapsed * 1e3 / args.steps
+    value = T / (ms / 1e3)
+    # average algorithmic units per step over the rotation actually timed
+    n = args.steps
+    avg = {k: sum(units[i % len(units)][k] for i in range(n)) / n for k in units[0]}
+    roof = None
+    if prof:
+        if decode:
+            name = "decode_gateup"
+            cnt, tot = prof.get(name, (0, 0.0))
+            if cnt:
+                dur = tot / cnt * 1e-3
+                achieved = avg["gu_bytes"] / dur / 1e9
+                roof = {"bound": "hbm", "kernel": name, "achieved": round(achieved, 1),
+                        "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                        "traffic": None, "avg_us": round(dur * 1e6, 2),
+                        "algorithmic_bytes_per_launch": int(avg["gu_bytes"])}
+        else:
+            name = "prefill_gateup"
+            cnt, tot = prof.get(name, (0, 0.0))
+            if cnt:
+                dur = tot / cnt * 1e-3
+                achieved = avg["gu_flops"] / dur / 1e12
+                roof = {"bound": "mfma", "kernel": name, "achieved": round(achieved, 1),
+                        "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                        "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": None,
+                        "avg_us": round(dur * 1e6, 2),
+                        "algorithmic_flops_per_launch": avg["gu_flops"]}
+    step_bytes = avg["gu_bytes"] + avg["dn_bytes"]
+    line = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "i8" if decode else "bf16",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "tokens": T, "hidden": cfg.C, "experts": cfg.E,
+                   "top_k": cfg.k, "ffn": cfg.R, "shared_experts": cfg.S,
+                   "activations": cfg.act, "layer_copies": len(copies),
+                   "experts_touched_per_step": round(avg["active"], 2)},
+        "step_packed_gbs": round(step_bytes / (ms / 1e3) / 1e9, 1),
+        "step_tflops": round((avg["gu_flops"] + avg["dn_flops"]) / (ms / 1e3) / 1e12, 2),
+        "kernels_us": {k: round(v[1] / v[0] * 1e3, 2) for k, v in prof.items() if v[0]},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(cfg, copies[0], args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

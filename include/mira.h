@@ -224,6 +224,9 @@ const char* mira_version(void);
  * launch count and the summed duration in milliseconds, then clears the
  * records.  Names are library-owned strings. */
 int mira_profile_enable(int32_t enable);
+/* Restrict the timing to kernels of one name (NULL or "" = all kernels), so
+ * that only the kernel under study carries event records. */
+int mira_profile_select(const char* kernel_name);
 int mira_profile_read(int32_t max_entries, const char** names, int32_t* counts,
                       double* total_ms, int32_t* n_entries);
 

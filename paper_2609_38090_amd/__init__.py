@@ -33,6 +33,7 @@ from ._binding import (  # noqa: F401
     mira_predict_workspace_bytes,
     mira_profile_enable,
     mira_profile_read,
+    mira_profile_select,
     mira_set_slot,
     mira_stage_expert,
     mira_version,
@@ -54,4 +55,5 @@ EXPORTED_SYMBOLS = (
     "mira_version",
     "mira_profile_enable",
     "mira_profile_read",
+    "mira_profile_select",
 )

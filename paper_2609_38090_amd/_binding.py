@@ -166,6 +166,7 @@ def load():
             "mira_last_error": (ctypes.c_char_p, []),
             "mira_version": (ctypes.c_char_p, []),
             "mira_profile_enable": (ctypes.c_int, [i32]),
+            "mira_profile_select": (ctypes.c_int, [ctypes.c_char_p]),
             "mira_profile_read": (ctypes.c_int, [i32, ctypes.POINTER(ctypes.c_char_p),
                                                  ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double),
                                                  ctypes.POINTER(i32)]),
@@ -251,6 +252,10 @@ def mira_set_slot(slot_table, expert: int, slot: int, stream=None):
 
 def mira_profile_enable(enable: bool = True):
     _check(load().mira_profile_enable(1 if enable else 0))
+
+
+def mira_profile_select(kernel_name=None):
+    _check(load().mira_profile_select(kernel_name.encode() if kernel_name else None))
 
 
 def mira_profile_read(max_entries: int = 64):

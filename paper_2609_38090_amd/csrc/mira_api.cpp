@@ -119,6 +119,13 @@ mira::ExpertPool pool_of(const mira_moe_args* a) {
 
 int run_route(const mira_shape* s, const mira_moe_args* a, const mira::Layout& L, hipStream_t st) {
   mira::WsPtr w = mira::ws_ptrs(L, a->workspace);
+  if (use_decode(*s, L.T)) {
+    // one workgroup: router, top-k, permutation and the digits of x
+    HIP_TRY(mira::launch_decode_prep(*s, L, w, a->x, a->w_router, a->router_bias, a->logits,
+                                     pool_of(a), a->expert_counts, a->topk_idx, a->topk_weight,
+                                     a->expert_offsets, a->pair_order, st));
+    return MIRA_OK;
+  }
   HIP_TRY(mira::launch_route(*s, L, w, a->x, a->w_router, a->router_bias, a->logits, st));
   HIP_TRY(mira::launch_permute(*s, L, w, pool_of(a), a->expert_counts, a->topk_idx,
                                a->topk_weight, a->expert_offsets, a->pair_order, st));
@@ -246,6 +253,7 @@ struct ProfRec {
 };
 std::mutex g_prof_mu;
 bool g_prof_on = false;
+std::string g_prof_only;
 std::vector<ProfRec> g_prof;
 std::vector<hipEvent_t> g_prof_free;
 
@@ -267,6 +275,7 @@ namespace mira {
 void prof_begin(const char* name, hipStream_t st) {
   std::lock_guard<std::mutex> g(g_prof_mu);
   if (!g_prof_on) return;
+  if (!g_prof_only.empty() && g_prof_only != name) return;
   ProfRec r{name, prof_event(), nullptr};
   if (r.a) hipEventRecord(r.a, st);
   g_prof.push_back(r);
@@ -275,6 +284,7 @@ void prof_begin(const char* name, hipStream_t st) {
 void prof_end(const char* name, hipStream_t st) {
   std::lock_guard<std::mutex> g(g_prof_mu);
   if (!g_prof_on) return;
+  if (!g_prof_only.empty() && g_prof_only != name) return;
   for (auto it = g_prof.rbegin(); it != g_prof.rend(); ++it) {
     if (it->b == nullptr && std::strcmp(it->name, name) == 0) {
       it->b = prof_event();
@@ -439,6 +449,12 @@ const char* mira_version(void) { return "mira-mi355x 0.1.0 (gfx950)"; }
 int mira_profile_enable(int32_t enable) {
   std::lock_guard<std::mutex> g(g_prof_mu);
   g_prof_on = enable != 0;
+  return MIRA_OK;
+}
+
+int mira_profile_select(const char* kernel_name) {
+  std::lock_guard<std::mutex> g(g_prof_mu);
+  g_prof_only = kernel_name ? kernel_name : "";
   return MIRA_OK;
 }
 

@@ -154,6 +154,11 @@ hipError_t launch_permute(const mira_shape& s, const Layout& L, const WsPtr& w,
                           const ExpertPool& ep, int32_t* counts_out, int32_t* idx_out,
                           float* wts_out, int32_t* offsets_out, int32_t* order_out,
                           hipStream_t st);
+hipError_t launch_decode_prep(const mira_shape& s, const Layout& L, const WsPtr& w, const void* x,
+                              const void* wr, const float* bias, float* logits_out,
+                              const ExpertPool& ep, int32_t* counts_out, int32_t* idx_out,
+                              float* wts_out, int32_t* offsets_out, int32_t* order_out,
+                              hipStream_t st);
 hipError_t launch_decode(const mira_shape& s, const Layout& L, const WsPtr& w, const void* x,
                          const ExpertPool& ep, float* out, hipStream_t st);
 hipError_t launch_prefill(const mira_shape& s, const Layout& L, const WsPtr& w, const void* x,
