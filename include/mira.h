@@ -81,7 +81,11 @@ typedef enum mira_dtype {
  *   2*R*C   int8  down [C][R]
  *   3*R*C   bf16  sigma[R]      (one scale per expert-hidden row r, shared by
  *                                gate row r, up row r and down column r)
- * zero-padded to a multiple of 256 bytes.  The dequantized weights are
+ * zero-padded to a multiple of 256 bytes.  Each int8 matrix [rows][K] is
+ * stored as tiles of 16 rows x 64 columns (1024 bytes), tile-rows in order and
+ * column blocks in order inside a tile-row; inside a tile, the 16-byte run
+ * number g*16 + i holds row i, columns 16g .. 16g+15.  So element (r, k) is at
+ *   ((r/16)*(K/64) + k/64)*1024 + ((k%64)/16*16 + r%16)*16 + k%16.  The dequantized weights are
  * sigma[r] * q.  Pack computes, per row r,
  *   alpha_r = max(|gate[r,:]|_inf, |up[r,:]|_inf, |down[:,r]|_inf)  (exact),
  *   s_r     = fl32(max(alpha_r, eps) / 127),

@@ -20,8 +20,9 @@ notes of the repository):
   follows the rounding.
 * Packed byte layout (section IV-B and the memory-layout figure only say the
   three INT8 matrices and the shared scale travel together): one blob per
-  expert, little-endian, int8 gate [R][C], int8 up [R][C], int8 down [C][R],
-  bf16 sigma [R], zero padding up to a multiple of 256 bytes.
+  expert, little-endian: int8 gate [R][C], int8 up [R][C], int8 down [C][R],
+  each stored as 16-row x 64-column tiles (see tile_order), then bf16 sigma
+  [R], zero padding up to a multiple of 256 bytes.
 * Matrix roles: the paper calls W1 the up projection and W3 the gate
   modulation without writing the FFN formula.  The library names matrices by
   role: "gate" goes through SiLU, "up" is the linear branch (Mixtral's w1 and
@@ -46,6 +47,8 @@ __all__ = [
     "bf16_bits_from_f32",
     "f32_from_bf16_bits",
     "packed_expert_bytes",
+    "tile_order",
+    "untile_order",
     "pack_expert",
     "unpack_expert",
     "dequantize_expert",
@@ -102,6 +105,29 @@ def packed_expert_bytes(C: int, R: int) -> int:
     return (raw + BLOB_ALIGN - 1) // BLOB_ALIGN * BLOB_ALIGN
 
 
+def tile_order(q):
+    """Byte order of one int8 matrix [rows][K] inside a blob.
+
+    The matrix is cut into tiles of 16 rows x 64 columns, stored tile-row by
+    tile-row and, inside a tile-row, by increasing column block.  Inside a
+    tile the 1024 bytes are 64 runs of 16 consecutive columns of one row; run
+    number g*16 + i holds row i of the tile, columns 16g .. 16g+15 of the
+    block.  rows must be a multiple of 16 and K of 64.
+    """
+    q = np.asarray(q)
+    rows, K = q.shape
+    if rows % 16 or K % 64:
+        raise ValueError("tiled layout needs rows % 16 == 0 and K % 64 == 0")
+    t = q.reshape(rows // 16, 16, K // 64, 4, 16)      # [tile-row][i][block][g][c]
+    return t.transpose(0, 2, 3, 1, 4).reshape(-1)        # [tile-row][block][g][i][c]
+
+
+def untile_order(flat, rows, K):
+    """Inverse of tile_order."""
+    t = np.asarray(flat).reshape(rows // 16, K // 64, 4, 16, 16)   # [tile-row][block][g][i][c]
+    return t.transpose(0, 3, 1, 2, 4).reshape(rows, K)
+
+
 def _shared_row_scale(w_gate, w_up, w_down, eps):
     """alpha_r, then s_r = max(alpha_r, eps) / 127 in fp32, then bf16 storage."""
     alpha = np.maximum(
@@ -133,6 +159,8 @@ def pack_expert(w_gate, w_up, w_down, eps=1e-8):
     R, C = w_gate.shape
     if w_up.shape != (R, C) or w_down.shape != (C, R):
         raise ValueError("expected gate/up [R][C] and down [C][R]")
+    if R % 64 or C % 64:
+        raise ValueError("C and R must be multiples of 64")
     if not (np.all(np.isfinite(w_gate)) and np.all(np.isfinite(w_up)) and np.all(np.isfinite(w_down))):
         raise ValueError("non-finite weights are out of contract")
     _, _, sigma_bits = _shared_row_scale(w_gate, w_up, w_down, eps)
@@ -145,7 +173,7 @@ def pack_expert(w_gate, w_up, w_down, eps=1e-8):
     o = 0
     for part in (q_gate, q_up, q_down):
         n = part.size
-        blob[o:o + n] = part.reshape(-1).view(np.uint8)
+        blob[o:o + n] = tile_order(part).view(np.uint8)
         o += n
     blob[o:o + 2 * R] = sigma_bits.astype("<u2").view(np.uint8)
     return blob
@@ -157,9 +185,9 @@ def unpack_expert(blob, C: int, R: int):
     if blob.size < 3 * R * C + 2 * R:
         raise ValueError("blob too small for the given shape")
     rc = R * C
-    q_gate = blob[0:rc].view(np.int8).reshape(R, C)
-    q_up = blob[rc:2 * rc].view(np.int8).reshape(R, C)
-    q_down = blob[2 * rc:3 * rc].view(np.int8).reshape(C, R)
+    q_gate = untile_order(blob[0:rc].view(np.int8), R, C)
+    q_up = untile_order(blob[rc:2 * rc].view(np.int8), R, C)
+    q_down = untile_order(blob[2 * rc:3 * rc].view(np.int8), C, R)
     sigma_bits = blob[3 * rc:3 * rc + 2 * R].view("<u2").astype(np.uint16)
     return q_gate, q_up, q_down, sigma_bits
 

@@ -36,39 +36,42 @@ __device__ __forceinline__ float combine_digits_i(int s0) {
 __host__ __device__ constexpr int dec_unroll(int ng) { return ng <= 2 ? 4 : 2; }
 
 template <int NG>
-__global__ __launch_bounds__(256) void decode_gateup_kernel(
-    int C, int R, ExpertPool ep, const int32_t* __restrict__ misc,
-    const int32_t* __restrict__ active, const int32_t* __restrict__ offsets,
-    const int32_t* __restrict__ tokpos, const int8_t* __restrict__ xdig,
-    const int32_t* __restrict__ xexp, int8_t* __restrict__ hdig, int32_t* __restrict__ hexp) {
+__global__ __launch_bounds__(256) void decode_gateup_kernel(int C, int R, ExpertPool ep,
+                                                            const DecodeWork* __restrict__ work,
+                                                            const int8_t* __restrict__ xdig,
+                                                            int8_t* __restrict__ hdig,
+                                                            int32_t* __restrict__ hexp) {
   __shared__ float bmax[4][NG * kTokPerGroup];
   const int nrb = R / kBlk;
   const int a = blockIdx.x / nrb, rb = blockIdx.x - a * nrb;
-  if (a >= misc[MISC_NACTIVE]) return;
-  const int g = active[a];
-  const int off = offsets[g], n = offsets[g + 1] - off;
-  const int slot = ep.slot_table[g];
+  const DecodeWork& wk = work[a];
+  const int g = wk.group;
+  if (g < 0) return;
+  const int slot = ep.slot_table[g];  // read now: the table may change after routing
   if (slot < 0 || slot >= ep.n_slots) {
     if (threadIdx.x == 0 && ep.status) atomicOr(ep.status, slot < 0 ? 1 : 2);
     return;
   }
+  const int off = wk.off, n = wk.n;
   const int8_t* blob = ep.pool + (size_t)slot * ep.stride;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kg = lane >> 4;
-  const int row = rb * kBlk + wave * 16 + r16;
-  const int8_t* gp = blob + (size_t)row * C + kg * 16;
+  // this wave's 16-row tile: 1 KB per k-step, lane l at byte 16*l
+  const int rtile = rb * (kBlk / 16) + wave;
+  const int8_t* gp = blob + (size_t)rtile * (C / 64) * 1024 + lane * 16;
   const int8_t* up = gp + (size_t)R * C;
 
   const int m = r16 / 3, d = r16 - 3 * m;
   const int8_t* bp[NG];
   bool bv[NG];
-  int tokv[NG];
+  int xev[NG];
 #pragma unroll
   for (int cg = 0; cg < NG; ++cg) {
     const int i = cg * kTokPerGroup + m;
     bv[cg] = r16 < 3 * kTokPerGroup && i < n;
-    tokv[cg] = bv[cg] ? tokpos[off + i] : 0;
-    bp[cg] = xdig + ((size_t)tokv[cg] * kDigits + d) * C + kg * 16;
+    const int tok = bv[cg] ? wk.tok[i] : 0;
+    xev[cg] = bv[cg] ? wk.xe[i] : 0;
+    bp[cg] = xdig + ((size_t)tok * kDigits + d) * C + kg * 16;
   }
 
   v4i accg[NG], accu[NG];
@@ -86,8 +89,8 @@ __global__ __launch_bounds__(256) void decode_gateup_kernel(
     for (int u = 0; u < kDecUnroll; ++u) {
       const int ks = ks0 + u;
       const bool in = ks < nks;
-      bt.ag[u] = in ? ld16_stream(gp + ks * 64) : zero16();
-      bt.au[u] = in ? ld16_stream(up + ks * 64) : zero16();
+      bt.ag[u] = in ? ld16_stream(gp + ks * 1024) : zero16();
+      bt.au[u] = in ? ld16_stream(up + ks * 1024) : zero16();
 #pragma unroll
       for (int cg = 0; cg < NG; ++cg) bt.b[u][cg] = (in && bv[cg]) ? ld16(bp[cg] + ks * 64) : zero16();
     }
@@ -119,7 +122,7 @@ __global__ __launch_bounds__(256) void decode_gateup_kernel(
   float hv[NG][4];
 #pragma unroll
   for (int cg = 0; cg < NG; ++cg) {
-    const float xs = bv[cg] ? ldexpf(1.f, -xexp[tokv[cg]]) : 0.f;
+    const float xs = bv[cg] ? ldexpf(1.f, -xev[cg]) : 0.f;
     float mx = 0.f;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -170,30 +173,28 @@ __global__ __launch_bounds__(256) void decode_gateup_kernel(
 // ---------------------------------------------------------------------------
 template <int NG, int KS>
 __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
-    int C, int R, int T, ExpertPool ep, const int32_t* __restrict__ misc,
-    const int32_t* __restrict__ active, const int32_t* __restrict__ offsets,
-    const int32_t* __restrict__ tokpos, const float* __restrict__ wpos,
+    int C, int R, int T, int max_active, ExpertPool ep, const DecodeWork* __restrict__ work,
     const int8_t* __restrict__ hdig, const int32_t* __restrict__ hexp, float* __restrict__ out) {
   __shared__ float part[KS][MIRA_DECODE_MAX_TOKENS][16];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   for (int i = tid; i < KS * MIRA_DECODE_MAX_TOKENS * 16; i += 64 * KS) (&part[0][0][0])[i] = 0.f;
   __syncthreads();
 
-  const int c0 = blockIdx.x * 16;
   const int r16 = lane & 15, kg = lane >> 4;
   const int m = r16 / 3, d = r16 - 3 * m;
   const int nks = R / 64;
   const int spw = (nks + KS - 1) / KS;
   const int ks_beg = wave * spw, ks_end = min(nks, ks_beg + spw);
-  const int na = misc[MISC_NACTIVE];
 
-  for (int a = 0; a < na; ++a) {
-    const int g = active[a];
-    const int off = offsets[g], n = offsets[g + 1] - off;
+  for (int a = 0; a < max_active; ++a) {
+    const DecodeWork& wk = work[a];
+    const int g = wk.group;
+    if (g < 0) break;
     const int slot = ep.slot_table[g];
     if (slot < 0 || slot >= ep.n_slots) continue;
+    const int off = wk.off, n = wk.n;
     const int8_t* dp = ep.pool + (size_t)slot * ep.stride + (size_t)2 * R * C +
-                       (size_t)(c0 + r16) * R + kg * 16;
+                       (size_t)blockIdx.x * nks * 1024 + lane * 16;  // tile row c0/16
     const int8_t* bp[NG];
     const int32_t* hx[NG];
     bool bv[NG];
@@ -221,7 +222,7 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
       for (int u = 0; u < kDecUnroll; ++u) {
         const int ks = ks0 + u;
         const bool in = ks < ks_end;
-        bt.a[u] = in ? ld16_stream(dp + ks * 64) : zero16();
+        bt.a[u] = in ? ld16_stream(dp + ks * 1024) : zero16();
 #pragma unroll
         for (int cg = 0; cg < NG; ++cg) {
           bt.b[u][cg] = (in && bv[cg]) ? ld16(bp[cg] + ks * 64) : zero16();
@@ -251,8 +252,8 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
     for (int cg = 0; cg < NG; ++cg) {
       const int ti = cg * kTokPerGroup + m;
       const bool lead = d == 0 && bv[cg];
-      const int t = lead ? tokpos[off + ti] : 0;
-      const float wgt = lead ? wpos[off + ti] : 0.f;
+      const int t = lead ? wk.tok[ti] : 0;
+      const float wgt = lead ? wk.w[ti] : 0.f;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float v = facc[cg][i] + __shfl_down(facc[cg][i], 1, 64) +
@@ -267,7 +268,7 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
     float s = 0.f;
 #pragma unroll
     for (int w = 0; w < KS; ++w) s += part[w][t][r];
-    out[(size_t)t * C + c0 + r] = s;
+    out[(size_t)t * C + blockIdx.x * 16 + r] = s;
   }
 }
 
@@ -277,16 +278,14 @@ template <int NG>
 static void launch_decode_ffn(const Layout& L, const WsPtr& w, const ExpertPool& ep, float* out,
                               hipStream_t st) {
   const int nrb = L.R / kBlk;
-  const int max_active = L.G < L.T * L.k + L.S ? L.G : L.T * L.k + L.S;
+  const int max_active = decode_max_active(L);
   prof_begin("decode_gateup", st);
-  hipLaunchKernelGGL(decode_gateup_kernel<NG>, dim3(max_active * nrb), dim3(256), 0, st, L.C,
-                     L.R, ep, w.misc, w.active, w.offsets, w.tokpos, w.xdig, w.xexp, w.hdig,
-                     w.hexp);
+  hipLaunchKernelGGL(decode_gateup_kernel<NG>, dim3(max_active * nrb), dim3(256), 0, st, L.C, L.R,
+                     ep, w.dwork, w.xdig, w.hdig, w.hexp);
   prof_end("decode_gateup", st);
   prof_begin("decode_down", st);
   hipLaunchKernelGGL((decode_down_kernel<NG, kDownKS>), dim3(L.C / 16), dim3(64 * kDownKS), 0, st,
-                     L.C, L.R, L.T, ep, w.misc, w.active, w.offsets, w.tokpos, w.wpos, w.hdig,
-                     w.hexp, out);
+                     L.C, L.R, L.T, max_active, ep, w.dwork, w.hdig, w.hexp, out);
   prof_end("decode_down", st);
 }
 

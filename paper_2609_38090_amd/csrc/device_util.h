@@ -31,6 +31,19 @@ __device__ __forceinline__ float load_act<uint16_t>(const uint16_t* p, size_t i)
   return bf16_to_f32(p[i]);
 }
 
+// four consecutive activations (16-byte or 8-byte aligned) widened to fp32
+__device__ __forceinline__ void load4_act(const float* p, float v[4]) {
+  const v4f q = *(const v4f*)p;
+  v[0] = q[0]; v[1] = q[1]; v[2] = q[2]; v[3] = q[3];
+}
+__device__ __forceinline__ void load4_act(const uint16_t* p, float v[4]) {
+  const uint2 q = *(const uint2*)p;
+  v[0] = __uint_as_float(q.x << 16);
+  v[1] = __uint_as_float(q.x & 0xFFFF0000u);
+  v[2] = __uint_as_float(q.y << 16);
+  v[3] = __uint_as_float(q.y & 0xFFFF0000u);
+}
+
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));

@@ -72,10 +72,14 @@ int check_shape(const mira_shape* s) {
   return MIRA_OK;
 }
 
+bool decode_fits(const mira_shape& s, int T) {
+  return T <= MIRA_DECODE_MAX_TOKENS && T * (s.top_k + s.n_shared) <= mira::kDecodeMaxPairs;
+}
+
 bool use_decode(const mira_shape& s, int T) {
   if (s.flags & MIRA_FLAG_FORCE_DECODE) return true;
   if (s.flags & MIRA_FLAG_FORCE_PREFILL) return false;
-  return T <= MIRA_DECODE_MAX_TOKENS;
+  return decode_fits(s, T);
 }
 
 int check_args(const mira_shape* s, const mira_moe_args* a, mira::Layout* L) {
@@ -83,9 +87,10 @@ int check_args(const mira_shape* s, const mira_moe_args* a, mira::Layout* L) {
   if (rc) return rc;
   if (!a) return fail(MIRA_ERR_ARG, "args is NULL");
   if (a->n_tokens < 0) return fail(MIRA_ERR_SHAPE, "n_tokens must be >= 0");
-  if ((s->flags & MIRA_FLAG_FORCE_DECODE) && a->n_tokens > MIRA_DECODE_MAX_TOKENS)
-    return fail(MIRA_ERR_SHAPE, "FORCE_DECODE needs n_tokens <= %d (got %d)",
-                MIRA_DECODE_MAX_TOKENS, a->n_tokens);
+  if ((s->flags & MIRA_FLAG_FORCE_DECODE) && !decode_fits(*s, a->n_tokens))
+    return fail(MIRA_ERR_SHAPE,
+                "FORCE_DECODE needs n_tokens <= %d and n_tokens * (top_k + n_shared) <= %d "
+                "(got %d tokens)", MIRA_DECODE_MAX_TOKENS, mira::kDecodeMaxPairs, a->n_tokens);
   if ((int64_t)a->n_tokens * (s->top_k + s->n_shared) > (int64_t)1 << 30)
     return fail(MIRA_ERR_SHAPE, "too many tokens");
   *L = mira::make_layout(*s, a->n_tokens);
@@ -227,15 +232,15 @@ void host_pack_one(int C, int R, const WT* wg, const WT* wu, const WT* wd, float
     for (int64_t i = b; i < e; ++i) {
       const int mat = (int)(i / R), r = (int)(i % R);
       const WT* src = (mat == 0 ? wg : wu) + (size_t)r * C;
-      int8_t* dst = blob + (size_t)mat * R * C + (size_t)r * C;
-      for (int c = 0; c < C; ++c) dst[c] = h_quant(h_ld(src, c), sigma[r]);
+      int8_t* dst = blob + (size_t)mat * R * C;
+      for (int c = 0; c < C; ++c) dst[mira::tiled_offset(r, c, C)] = h_quant(h_ld(src, c), sigma[r]);
     }
   });
   parallel_for(C, [&](int64_t b, int64_t e) {
-    for (int64_t c = b; c < e; ++c) {
-      int8_t* dst = blob + (size_t)2 * R * C + (size_t)c * R;
-      for (int r = 0; r < R; ++r) dst[r] = h_quant(h_ld(wd, (size_t)c * R + r), sigma[r]);
-    }
+    int8_t* dst = blob + (size_t)2 * R * C;
+    for (int64_t c = b; c < e; ++c)
+      for (int r = 0; r < R; ++r)
+        dst[mira::tiled_offset(c, r, R)] = h_quant(h_ld(wd, (size_t)c * R + r), sigma[r]);
   });
   uint8_t* sig = (uint8_t*)(blob + (size_t)3 * R * C);
   for (int r = 0; r < R; ++r) {

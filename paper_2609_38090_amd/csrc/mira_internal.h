@@ -21,6 +21,16 @@ constexpr int kPrefBM = 64;          // prefill tile: tokens per m-tile (shared 
 
 inline __host__ __device__ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
+// Packed int8 matrices [rows][K] are stored as 16-row x 64-column tiles of
+// 1024 bytes, row-of-tiles major; inside a tile, 16-byte run g*16 + i holds
+// row i, columns 16g .. 16g+15.  One wave's 128-bit loads of a tile are one
+// contiguous kilobyte and land exactly in the int8 MFMA operand layout
+// (lane l = row l%16, k-group l/16).
+inline __host__ __device__ size_t tiled_offset(size_t r, size_t k, size_t K) {
+  return (((r >> 4) * (K >> 6) + (k >> 6)) << 10) + ((((k & 63) >> 4) << 4 | (r & 15)) << 4) +
+         (k & 15);
+}
+
 // ---------------------------------------------------------------------------
 // Workspace layout of one call with T tokens.  Every region is 256-aligned.
 // Decode regions are sized for min(T, MIRA_DECODE_MAX_TOKENS) tokens.
@@ -31,12 +41,32 @@ struct Layout {
   int Pd;       // pairs of the decode sizing
   int Td;       // tokens of the decode sizing
   int mt_max;   // upper bound of prefill m-tiles
-  size_t logits, idx, wts, counts, offsets, inv, tokpos, wpos, misc, active, mstart, mtile_g,
-      mtile_m0, xdig, xexp, hdig, hexp, xb16, hbuf, ybuf, total;
+  size_t logits, idx, wts, counts, offsets, inv, tokpos, wpos, misc, active, mstart, dwork,
+      xdig, xexp, hdig, hexp, xb16, hbuf, ybuf, total;
 };
+
+// One non-empty expert group of a decode call, written by the decode
+// preparation kernel so that each expert kernel starts from a single load.
+struct DecodeWork {
+  int32_t group;  // expert (routed 0..E-1, shared E..E+S-1); -1 = no work
+  int32_t slot;   // slot seen by the routing (the expert kernels re-read the table)
+  int32_t off;    // first permuted position of the group
+  int32_t n;      // positions (tokens) of the group, <= MIRA_DECODE_MAX_TOKENS
+  int32_t tok[MIRA_DECODE_MAX_TOKENS];  // token of position off+i
+  int32_t xe[MIRA_DECODE_MAX_TOKENS];   // fixed-point exponent of that token's x
+  float w[MIRA_DECODE_MAX_TOKENS];      // combine weight of position off+i
+};
+
+// Largest number of (token, slot) pairs the decode preparation handles.
+constexpr int kDecodeMaxPairs = 1024;
 
 // misc[] slots (int32)
 enum : int { MISC_NACTIVE = 0, MISC_MTOTAL = 1, MISC_COUNT = 16 };
+
+inline int decode_max_active_of(int G, int T, int k, int S) {
+  const int pairs_groups = T * k + S;
+  return G < pairs_groups ? G : pairs_groups;
+}
 
 inline Layout make_layout(const mira_shape& s, int T) {
   Layout L{};
@@ -69,8 +99,7 @@ inline Layout make_layout(const mira_shape& s, int T) {
   L.misc = take(MISC_COUNT * 4);
   L.active = take(G * 4);
   L.mstart = take((G + 1) * 4);
-  L.mtile_g = take((size_t)L.mt_max * 4);
-  L.mtile_m0 = take((size_t)L.mt_max * 4);
+  L.dwork = take(G * sizeof(DecodeWork));
   L.xdig = take((size_t)L.Td * kDigits * L.C);
   L.xexp = take((size_t)L.Td * 4);
   L.hdig = take((size_t)L.Pd * kDigits * L.R);
@@ -95,8 +124,7 @@ struct WsPtr {
   int32_t* misc;
   int32_t* active;
   int32_t* mstart;
-  int32_t* mtile_g;
-  int32_t* mtile_m0;
+  DecodeWork* dwork;
   int8_t* xdig;
   int32_t* xexp;
   int8_t* hdig;
@@ -120,8 +148,7 @@ inline WsPtr ws_ptrs(const Layout& L, void* base) {
   w.misc = (int32_t*)(b + L.misc);
   w.active = (int32_t*)(b + L.active);
   w.mstart = (int32_t*)(b + L.mstart);
-  w.mtile_g = (int32_t*)(b + L.mtile_g);
-  w.mtile_m0 = (int32_t*)(b + L.mtile_m0);
+  w.dwork = (DecodeWork*)(b + L.dwork);
   w.xdig = (int8_t*)(b + L.xdig);
   w.xexp = (int32_t*)(b + L.xexp);
   w.hdig = (int8_t*)(b + L.hdig);
@@ -131,6 +158,8 @@ inline WsPtr ws_ptrs(const Layout& L, void* base) {
   w.ybuf = (float*)(b + L.ybuf);
   return w;
 }
+
+inline int decode_max_active(const Layout& L) { return decode_max_active_of(L.G, L.T, L.k, L.S); }
 
 // Everything the expert kernels need to find a packed expert.
 struct ExpertPool {

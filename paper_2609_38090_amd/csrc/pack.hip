@@ -60,7 +60,7 @@ __device__ __forceinline__ int8_t quant(float w, float sigma) {
   return (int8_t)(int)q;
 }
 
-// gate/up rows: blob[e] bytes [0, 2RC); one workgroup per (row, matrix)
+// gate/up rows: blob[e] bytes [0, 2RC) in the tiled layout; one workgroup per (row, matrix)
 template <typename WT>
 __global__ __launch_bounds__(256) void pack_quant_rows_kernel(const WT* __restrict__ wg,
                                                               const WT* __restrict__ wu, int C,
@@ -71,8 +71,8 @@ __global__ __launch_bounds__(256) void pack_quant_rows_kernel(const WT* __restri
   const int e = blockIdx.z, mat = blockIdx.y, r = blockIdx.x;
   const float sigma = scale_of(amax[(size_t)e * R + r], eps);
   const WT* src = (mat == 0 ? wg : wu) + ((size_t)e * R + r) * C;
-  int8_t* dst = packed + (size_t)e * stride + (size_t)mat * R * C + (size_t)r * C;
-  for (int c = threadIdx.x; c < C; c += 256) dst[c] = quant(ldw(src, c), sigma);
+  int8_t* dst = packed + (size_t)e * stride + (size_t)mat * R * C;
+  for (int c = threadIdx.x; c < C; c += 256) dst[tiled_offset(r, c, C)] = quant(ldw(src, c), sigma);
 }
 
 // down [C][R]: column r uses sigma_r; also writes sigma and zero padding
@@ -87,7 +87,7 @@ __global__ __launch_bounds__(256) void pack_quant_down_kernel(const WT* __restri
   if (r >= R) return;
   const float sigma = scale_of(amax[(size_t)e * R + r], eps);
   int8_t* blob = packed + (size_t)e * stride;
-  blob[(size_t)2 * R * C + (size_t)c * R + r] = quant(ldw(wd, ((size_t)e * C + c) * R + r), sigma);
+  blob[(size_t)2 * R * C + tiled_offset(c, r, R)] = quant(ldw(wd, ((size_t)e * C + c) * R + r), sigma);
   if (c == 0) {
     uint16_t* sig = (uint16_t*)(blob + (size_t)3 * R * C);
     sig[r] = f32_to_bf16_rne(fmaxf(__uint_as_float(amax[(size_t)e * R + r]), eps) / 127.0f);

@@ -91,15 +91,18 @@ __global__ __launch_bounds__(kGemmThreads) void prefill_gemm_kernel(
     const int8_t* blob = ep.pool + (size_t)slot * ep.stride;
     const int8_t* wbase = blob + (DUAL ? 0 : (size_t)2 * R * C);
 
-    // per-thread global sources of this tile
+    // per-thread global sources of this tile.  Weight chunks walk whole
+    // 1 KB tiles of the packed layout (16 rows x 64 k, run g*16+i = row i,
+    // k 16g..16g+15), so consecutive lanes read consecutive 16 bytes.
     const int8_t* wsrc[WC_PER_T];
     int wdst[WC_PER_T];
 #pragma unroll
     for (int i = 0; i < WC_PER_T; ++i) {
       const int ch = tid + i * kGemmThreads;
-      const int row = ch / (kBK / 16), part = ch - row * (kBK / 16);  // row < NB*BN
-      const int mat = row / BN, rr = row - mat * BN;
-      wsrc[i] = wbase + (size_t)mat * R * C + (size_t)(n0 + rr) * K + part * 16;
+      const int tl = ch >> 6, run = ch & 63;                    // tile of the stage, run in it
+      const int mat = tl / (BN / 16), rt = tl - mat * (BN / 16);
+      const int row = mat * BN + rt * 16 + (run & 15), part = run >> 4;
+      wsrc[i] = wbase + (size_t)mat * R * C + (size_t)(n0 / 16 + rt) * (K / 64) * 1024 + run * 16;
       wdst[i] = ch < W_CHUNKS ? row * kLdsRow + part * 16 : -1;
     }
     const uint16_t* xsrc[XC_PER_T];
@@ -127,7 +130,8 @@ __global__ __launch_bounds__(kGemmThreads) void prefill_gemm_kernel(
     v4i wreg[WC_PER_T], xreg[XC_PER_T];
     auto gload = [&](int k0) {
 #pragma unroll
-      for (int i = 0; i < WC_PER_T; ++i) wreg[i] = wdst[i] >= 0 ? ld16_stream(wsrc[i] + k0) : zero16();
+      for (int i = 0; i < WC_PER_T; ++i)
+        wreg[i] = wdst[i] >= 0 ? ld16_stream(wsrc[i] + (size_t)(k0 >> 6) * 1024) : zero16();
 #pragma unroll
       for (int i = 0; i < XC_PER_T; ++i) xreg[i] = xok[i] ? ld16(xsrc[i] + k0) : zero16();
     };

@@ -84,109 +84,107 @@ __device__ __forceinline__ void logits_tile_f32(const float* __restrict__ x,
 
 // Decode variant for bf16: all waves of the workgroup split the k range of
 // every expert tile; partial sums are reduced through LDS in wave order.
+__device__ __forceinline__ float absmax_bf16x8(v4i v) {
+  float m = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t u = (uint32_t)v[i];
+    m = fmaxf(m, fmaxf(fabsf(__uint_as_float(u << 16)), fabsf(__uint_as_float(u & 0xFFFF0000u))));
+  }
+  return m;
+}
+
+// (also writes max |x[t][:]| of each token into xmax[t]; bias_s is the
+// router bias, staged into LDS by pre_sync() right before the first barrier)
+template <typename PreSync>
 __device__ void logits_ksplit_bf16(const uint16_t* __restrict__ x, const uint16_t* __restrict__ wr,
-                                   const float* __restrict__ bias, int T, int E, int C,
-                                   float (*part)[16][17], float (*lg)[MIRA_MAX_EXPERTS]) {
+                                   const float* bias_s, int T, int E, int C,
+                                   float (*part)[16][17], float (*lg)[MIRA_MAX_EXPERTS],
+                                   float* xmax, PreSync pre_sync) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, kg = lane >> 4;
   const int n_et = (E + 15) / 16, nch = C / 32;
   const bool tok_ok = r16 < T;
   const uint16_t* xrow = x + (size_t)(tok_ok ? r16 : 0) * C + kg * 8;
+  constexpr int B = 8;  // chunks in flight per wave
   for (int et = 0; et < n_et; ++et) {
     const int e = et * 16 + r16;
     const bool e_ok = e < E;
     const uint16_t* wrow = wr + (size_t)(e_ok ? e : 0) * C + kg * 8;
     v4f acc = {0.f, 0.f, 0.f, 0.f};
-    int ch = wave;
-    for (; ch + 3 * kBigWaves < nch; ch += 4 * kBigWaves) {
-      v4i a[4], b[4];
+    float xm = 0.f;
+    for (int ch0 = wave; ch0 < nch; ch0 += B * kBigWaves) {
+      v4i a[B], b[B];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        a[u] = e_ok ? ld16(wrow + (ch + u * kBigWaves) * 32) : zero16();
-        b[u] = tok_ok ? ld16(xrow + (ch + u * kBigWaves) * 32) : zero16();
+      for (int u = 0; u < B; ++u) {
+        const int ch = ch0 + u * kBigWaves;
+        const bool in = ch < nch;
+        a[u] = (in && e_ok) ? ld16(wrow + ch * 32) : zero16();
+        b[u] = (in && tok_ok) ? ld16(xrow + ch * 32) : zero16();
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u) acc = mfma_bf16(a[u], b[u], acc);
-    }
-    for (; ch < nch; ch += kBigWaves) {
-      v4i a = e_ok ? ld16(wrow + ch * 32) : zero16();
-      v4i b = tok_ok ? ld16(xrow + ch * 32) : zero16();
-      acc = mfma_bf16(a, b, acc);
+      for (int u = 0; u < B; ++u) {
+        acc = mfma_bf16(a[u], b[u], acc);
+        if (et == 0) xm = fmaxf(xm, absmax_bf16x8(b[u]));
+      }
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) part[wave][r16][kg * 4 + i] = acc[i];  // [token][expert]
+    if (et == 0) {
+      // this wave's max over its chunks of token r16: combine the 4 lane groups
+      xm = fmaxf(xm, __shfl_xor(xm, 16, 64));
+      xm = fmaxf(xm, __shfl_xor(xm, 32, 64));
+      if (kg == 0) part[wave][r16][16] = xm;  // column 16 is spare
+      pre_sync();  // caller's LDS staging, issued before the loads above
+    }
     __syncthreads();
+    if (et == 0 && tid < 16) {
+      float m = 0.f;
+      for (int w = 0; w < kBigWaves; ++w) m = fmaxf(m, part[w][tid][16]);
+      xmax[tid] = m;
+    }
     if (tid < 256) {
       const int tt = tid >> 4, ee = tid & 15, e2 = et * 16 + ee;
       float s = 0.f;
       for (int w = 0; w < kBigWaves; ++w) s += part[w][tt][ee];
-      if (e2 < E) lg[tt][e2] = s + (bias ? bias[e2] : 0.f);
+      if (e2 < E) lg[tt][e2] = s + (bias_s ? bias_s[e2] : 0.f);
     }
     __syncthreads();
   }
 }
 
-// ---------------------------------------------------------------------------
-// Top-k of one token (one wave): repeatedly take the largest key (value,
-// then the lower index), then the combine weights.  Lanes j < k write
-// selection j.
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ void topk_token(const float* __restrict__ lgrow, int E, int k,
-                                           int softmax_all, int32_t* idx_a, float* w_a,
-                                           int32_t* idx_b, float* w_b) {
+// Top-k of one token by rank counting (one wave): expert e is selected at
+// position rank(e) = number of experts with a larger (value, then lower
+// index) key, if that is < k.  Every lane reads the logits by LDS broadcast,
+// so no cross-lane shuffles are needed.  sel_e/sel_v: this wave's LDS scratch.
+__device__ __forceinline__ void topk_rank(const float* lgrow, int E, int k, int softmax_all,
+                                          int32_t* idx_a, float* w_a, int* sel_e, float* sel_v) {
   const int lane = threadIdx.x & 63;
-  uint32_t khi[MIRA_MAX_EXPERTS / 64], klo[MIRA_MAX_EXPERTS / 64];
-#pragma unroll
-  for (int i = 0; i < MIRA_MAX_EXPERTS / 64; ++i) {
-    const int e = lane + 64 * i;
-    khi[i] = e < E ? f32_order_key(lgrow[e]) : 0u;
-    klo[i] = e < E ? ~(uint32_t)e : 0u;
-  }
-  int my_e = 0;
-  float my_v = 0.f;
-  for (int j = 0; j < k; ++j) {
-    uint32_t bh = 0, bl = 0;
-#pragma unroll
-    for (int i = 0; i < MIRA_MAX_EXPERTS / 64; ++i)
-      if (khi[i] > bh || (khi[i] == bh && klo[i] > bl)) {
-        bh = khi[i];
-        bl = klo[i];
-      }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-      const uint32_t oh = __shfl_xor(bh, o, 64), ol = __shfl_xor(bl, o, 64);
-      if (oh > bh || (oh == bh && ol > bl)) {
-        bh = oh;
-        bl = ol;
-      }
+  for (int e = lane; e < E; e += 64) {
+    const uint32_t ke = f32_order_key(lgrow[e]);
+    int rank = 0;
+    for (int e2 = 0; e2 < E; ++e2) {
+      const uint32_t k2 = f32_order_key(lgrow[e2]);
+      rank += (k2 > ke) || (k2 == ke && e2 < e);
     }
-    const int e_sel = (int)~bl;
-    if (lane == j) {
-      my_e = e_sel;
-      my_v = lgrow[e_sel];
-    }
-    if (lane == (e_sel & 63)) {
-#pragma unroll
-      for (int i = 0; i < MIRA_MAX_EXPERTS / 64; ++i)
-        if (i == (e_sel >> 6)) khi[i] = klo[i] = 0u;
+    if (rank < k) {
+      sel_e[rank] = e;
+      sel_v[rank] = lgrow[e];
     }
   }
-  const float vmax = __shfl(my_v, 0, 64);
-  const float ex = lane < k ? expf(my_v - vmax) : 0.f;
-  float denom;
+  __builtin_amdgcn_wave_barrier();
+  const float vmax = sel_v[0];
+  float denom = 0.f;
   if (softmax_all) {
     float s = 0.f;
     for (int e = lane; e < E; e += 64) s += expf(lgrow[e] - vmax);
     denom = wave_sum(s);
   } else {
-    denom = wave_sum(ex);
+    for (int j = 0; j < k; ++j) denom += expf(sel_v[j] - vmax);
   }
   if (lane < k) {
-    const float w = ex / denom;
-    idx_a[lane] = my_e;
-    w_a[lane] = w;
-    if (idx_b) idx_b[lane] = my_e;
-    if (w_b) w_b[lane] = w;
+    idx_a[lane] = sel_e[lane];
+    w_a[lane] = expf(sel_v[lane] - vmax) / denom;
   }
 }
 
@@ -196,6 +194,8 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
     int T, int E, int C, int k, int softmax_all, float* __restrict__ logits_ws,
     float* __restrict__ logits_out, int32_t* __restrict__ idx_ws, float* __restrict__ w_ws) {
   __shared__ float lg[kRouteTok][MIRA_MAX_EXPERTS];
+  __shared__ int sel_e[kRouteThreads / 64][MIRA_MAX_TOPK];
+  __shared__ float sel_v[kRouteThreads / 64][MIRA_MAX_TOPK];
   const int t0 = blockIdx.x * kRouteTok;
   if constexpr (sizeof(ActT) == 2)
     logits_tile_bf16(x, wr, bias, T, E, C, t0, kRouteThreads / 64, lg);
@@ -210,8 +210,9 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
       logits_ws[(size_t)t * E + e] = lg[tt][e];
       if (logits_out) logits_out[(size_t)t * E + e] = lg[tt][e];
     }
-    topk_token(lg[tt], E, k, softmax_all, idx_ws + (size_t)t * k, w_ws + (size_t)t * k, nullptr,
-               nullptr);
+    topk_rank(lg[tt], E, k, softmax_all, idx_ws + (size_t)t * k, w_ws + (size_t)t * k, sel_e[wave],
+              sel_v[wave]);
+    __builtin_amdgcn_wave_barrier();  // sel scratch is reused by this wave's next token
   }
 }
 
@@ -415,8 +416,165 @@ __global__ __launch_bounds__(kBigThreads) void permute_kernel(const int32_t* __r
 }
 
 // ---------------------------------------------------------------------------
-// Decode preparation (T <= 16 tokens, one workgroup): router logits, top-k
-// and weights, permutation, and the fixed-point digits of x used by the
+// Stable grouping for a decode call (T <= 16 tokens, at most kDecodeMaxPairs
+// pairs) by one wave: chunks of 64 pairs in order, ranks from ballots, running
+// group bases in LDS.  Same outputs as permute_body, plus one DecodeWork
+// descriptor per non-empty group.
+// ---------------------------------------------------------------------------
+__device__ void permute_decode_wave(const int32_t* idx, const float* wts, const int* xe_s,
+                                    const int* slot_s, int T, int k, int E, int S,
+                                    const ExpertPool& ep, const PermOut& o,
+                                    DecodeWork* __restrict__ work, int max_active, int* cnt_s,
+                                    int* run_s, int* ptok_s, float* pw_s) {
+  // reused once the counts and running bases are consumed: per non-empty group
+  int* act_off_s = cnt_s;
+  int* act_n_s = run_s;
+  const int lane = threadIdx.x & 63;
+  const int G = E + S, Tk = T * k;
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int g = lane; g < G; g += 64) cnt_s[g] = g >= E ? T : 0;
+  __builtin_amdgcn_wave_barrier();
+  auto match = [&](bool ok, int e) {
+    uint64_t same = __ballot(ok);
+#pragma unroll
+    for (int bit = 0; bit < 8; ++bit) {
+      const uint64_t bb = __ballot(ok && ((e >> bit) & 1));
+      same &= ((e >> bit) & 1) ? bb : ~bb;
+    }
+    return same;
+  };
+  for (int base = 0; base < Tk; base += 64) {
+    const int p = base + lane;
+    const bool ok = p < Tk;
+    const int e = ok ? idx[p] : 0;
+    const uint64_t same = match(ok, e);
+    if (ok && (same & lt_mask) == 0) cnt_s[e] += __popcll(same);
+    __builtin_amdgcn_wave_barrier();
+    if (ok) {
+      if (o.idx_out) o.idx_out[p] = e;
+      if (o.w_out) o.w_out[p] = wts[p];
+    }
+  }
+  // one exclusive scan over groups (4 consecutive groups per lane) carrying
+  // both the pair count (low 16 bits) and the non-empty group count (high)
+  int c4[4], sum = 0, nz = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int g = lane * 4 + i;
+    c4[i] = g < G ? cnt_s[g] : 0;
+    sum += c4[i];
+    nz += c4[i] > 0;
+  }
+  int packed = sum | (nz << 16);
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int v = __shfl_up(packed, off, 64);
+    if (lane >= off) packed += v;
+  }
+  const int incl = packed & 0xFFFF, ia = packed >> 16, na = nz;
+  int run = incl - sum;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int g = lane * 4 + i;
+    if (g < G) {
+      run_s[g] = run;
+      o.counts_ws[g] = c4[i];
+      o.offsets[g] = run;
+      if (o.counts_out) o.counts_out[g] = c4[i];
+      if (o.offsets_out) o.offsets_out[g] = run;
+    }
+    run += c4[i];
+  }
+  if (lane == 63) {
+    o.offsets[G] = incl;
+    if (o.offsets_out) o.offsets_out[G] = incl;
+  }
+  __builtin_amdgcn_wave_barrier();
+  // positions of routed pairs
+  for (int base = 0; base < Tk; base += 64) {
+    const int p = base + lane;
+    const bool ok = p < Tk;
+    const int e = ok ? idx[p] : 0;
+    const uint64_t same = match(ok, e);
+    int b0 = 0;
+    if (ok) b0 = run_s[e];
+    __builtin_amdgcn_wave_barrier();  // every lane has read its base
+    if (ok) {
+      const int pos = b0 + __popcll(same & lt_mask);
+      const float w = wts[p];
+      o.inv[p] = pos;
+      o.tokpos[pos] = p / k;
+      o.wpos[pos] = w;
+      ptok_s[pos] = p / k;
+      pw_s[pos] = w;
+      if (o.order_out) o.order_out[pos] = p;
+      if ((same & lt_mask) == 0) run_s[e] = b0 + __popcll(same);
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+  // shared experts: every token in order, weight 1 (their bases were not advanced)
+  for (int i = lane; i < S * T; i += 64) {
+    const int s = i / T, t = i - s * T;
+    const int pos = run_s[E + s] + t;
+    o.inv[Tk + i] = pos;
+    o.tokpos[pos] = t;
+    o.wpos[pos] = 1.0f;
+    ptok_s[pos] = t;
+    pw_s[pos] = 1.0f;
+    if (o.order_out) o.order_out[pos] = Tk + i;
+  }
+  __builtin_amdgcn_wave_barrier();
+  // non-empty groups in order -> descriptors (headers by the owning lane,
+  // then the per-position fields spread over all lanes)
+  const int n_active = __shfl(ia, 63, 64);
+  int ra = ia - na, bits = 0;
+  int gbase = incl - sum;
+  for (int i = 0; i < 4; ++i) {
+    const int g = lane * 4 + i;
+    if (g < G && c4[i] > 0) {
+      const int slot = slot_s[g];
+      if (slot < 0) bits |= 1;
+      else if (slot >= ep.n_slots) bits |= 2;
+      o.active[ra] = g;
+      DecodeWork* wk = work + ra;
+      wk->group = g;
+      wk->slot = slot;
+      wk->off = gbase;
+      wk->n = c4[i];
+      act_off_s[ra] = gbase;
+      act_n_s[ra] = c4[i];
+      ++ra;
+    }
+    gbase += c4[i];
+  }
+  __builtin_amdgcn_wave_barrier();
+  for (int it = lane; it < n_active * MIRA_DECODE_MAX_TOKENS; it += 64) {
+    const int a = it / MIRA_DECODE_MAX_TOKENS, j = it - a * MIRA_DECODE_MAX_TOKENS;
+    const int off = act_off_s[a];
+    const bool v = j < act_n_s[a];
+    const int t = v ? ptok_s[off + j] : 0;
+    work[a].tok[j] = t;
+    work[a].xe[j] = v ? xe_s[t] : 0;
+    work[a].w[j] = v ? pw_s[off + j] : 0.f;
+  }
+  for (int a = n_active + lane; a < max_active; a += 64) work[a].group = -1;
+  bits |= __shfl_xor(bits, 1, 64);
+  bits |= __shfl_xor(bits, 2, 64);
+  bits |= __shfl_xor(bits, 4, 64);
+  bits |= __shfl_xor(bits, 8, 64);
+  bits |= __shfl_xor(bits, 16, 64);
+  bits |= __shfl_xor(bits, 32, 64);
+  if (lane == 0) {
+    o.misc[MISC_NACTIVE] = n_active;
+    o.misc[MISC_MTOTAL] = 0;
+    if (ep.status) *ep.status = bits;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Decode preparation (T <= 16 tokens, one workgroup): router logits (with
+// max |x| per token on the way), top-k and weights; then wave 0 groups the
+// pairs while the other waves write the fixed-point digits of x used by the
 // integer expert kernels (|x * 2^E_t| < 2^22 per token, three signed
 // base-256 digits; layout xdig[(t*3 + d)*C + c], xexp[t] = E_t).
 // ---------------------------------------------------------------------------
@@ -424,53 +582,96 @@ template <typename ActT>
 __global__ __launch_bounds__(kBigThreads) void decode_prep_kernel(
     const ActT* __restrict__ x, const ActT* __restrict__ wr, const float* __restrict__ bias,
     int T, int E, int C, int k, int S, int softmax_all, float* __restrict__ logits_out,
-    ExpertPool ep, PermOut o, int8_t* __restrict__ xdig, int32_t* __restrict__ xexp) {
+    ExpertPool ep, PermOut o, DecodeWork* __restrict__ work, int max_active,
+    int8_t* __restrict__ xdig, int32_t* __restrict__ xexp) {
   __shared__ float lg[kRouteTok][MIRA_MAX_EXPERTS];
   __shared__ float part[kBigWaves][16][17];
   __shared__ int32_t idx_s[kRouteTok * MIRA_MAX_TOPK];
   __shared__ float w_s[kRouteTok * MIRA_MAX_TOPK];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __shared__ float xmax[kRouteTok];
+  __shared__ int xe_s[kRouteTok];
+  __shared__ int cnt_s[MIRA_MAX_EXPERTS], run_s[MIRA_MAX_EXPERTS];
+  __shared__ int ptok_s[kDecodeMaxPairs];
+  __shared__ float pw_s[kDecodeMaxPairs];
+  __shared__ float bias_s[MIRA_MAX_EXPERTS];
+  __shared__ int slot_s[MIRA_MAX_EXPERTS];
+  __shared__ int sel_e[kRouteTok][MIRA_MAX_TOPK];
+  __shared__ float sel_v[kRouteTok][MIRA_MAX_TOPK];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // load the router bias and the slot table into registers now and store
+  // them to LDS just before the logits barrier, so the loads overlap
+  float bias_r[MIRA_MAX_EXPERTS / kBigThreads + 1];
+  int slot_r[MIRA_MAX_EXPERTS / kBigThreads + 1];
+#pragma unroll
+  for (int i = 0; i <= MIRA_MAX_EXPERTS / kBigThreads; ++i) {
+    const int e = tid + i * kBigThreads;
+    bias_r[i] = (bias && e < E) ? bias[e] : 0.f;
+    slot_r[i] = e < E + S ? ep.slot_table[e] : 0;
+  }
+  auto stage = [&]() {
+#pragma unroll
+    for (int i = 0; i <= MIRA_MAX_EXPERTS / kBigThreads; ++i) {
+      const int e = tid + i * kBigThreads;
+      if (e < E) bias_s[e] = bias_r[i];
+      if (e < E + S) slot_s[e] = slot_r[i];
+    }
+  };
 
   if constexpr (sizeof(ActT) == 2) {
-    logits_ksplit_bf16(x, wr, bias, T, E, C, part, lg);
+    logits_ksplit_bf16(x, wr, bias_s, T, E, C, part, lg, xmax, stage);
   } else {
+    stage();
     logits_tile_f32(x, wr, bias, T, E, C, 0, kBigWaves, lg);
+    if (wave < T) {  // one wave per token: max |x|
+      float m = 0.f;
+      for (int c = lane * 4; c < C; c += 256) {
+        float v[4];
+        load4_act(x + (size_t)wave * C + c, v);
+        m = fmaxf(m, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
+      }
+      m = wave_max(m);
+      if (lane == 0) xmax[wave] = m;
+    }
     __syncthreads();
   }
   if (wave < T) {
     const int t = wave;
     if (logits_out)
       for (int e = lane; e < E; e += 64) logits_out[(size_t)t * E + e] = lg[t][e];
-    topk_token(lg[t], E, k, softmax_all, idx_s + t * k, w_s + t * k, nullptr, nullptr);
+    topk_rank(lg[t], E, k, softmax_all, idx_s + t * k, w_s + t * k, sel_e[t], sel_v[t]);
+  }
+  if (tid < T) {
+    const int Ex = kFixBits - exp_bound(xmax[tid]);
+    xe_s[tid] = Ex;
+    xexp[tid] = Ex;
   }
   __syncthreads();
-  permute_body(idx_s, w_s, T, k, E, S, kPrefBM, ep, o);
 
-  // fixed-point digits of x, one wave per token
-  if (wave < T) {
-    const int t = wave;
-    const ActT* xr = x + (size_t)t * C;
-    float m = 0.f;
-    for (int c = lane; c < C; c += 64) m = fmaxf(m, fabsf(load_act(xr, c)));
-    m = wave_max(m);
-    const int Ex = kFixBits - exp_bound(m);
-    int8_t* d0p = xdig + (size_t)t * kDigits * C;
-    for (int c = lane * 4; c < C; c += 256) {
-      uint32_t w0 = 0, w1 = 0, w2 = 0;
+  if (wave == 0) {
+    permute_decode_wave(idx_s, w_s, xe_s, slot_s, T, k, E, S, ep, o, work, max_active, cnt_s,
+                        run_s, ptok_s, pw_s);
+    return;
+  }
+  // waves 1..15: fixed-point digits of x, four elements per thread and step
+  const int q4 = C / 4, n4 = T * q4;
+  for (int i = tid - 64; i < n4; i += kBigThreads - 64) {
+    const int t = i / q4, c = (i - t * q4) * 4;
+    const int Ex = xe_s[t];
+    float v[4];
+    load4_act(x + (size_t)t * C + c, v);
+    uint32_t w0 = 0, w1 = 0, w2 = 0;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int v = (int)rintf(ldexpf(load_act(xr, c + i), Ex));
-        int d0, d1, d2;
-        split_digits(v, d0, d1, d2);
-        w0 |= (uint32_t)(d0 & 0xFF) << (8 * i);
-        w1 |= (uint32_t)(d1 & 0xFF) << (8 * i);
-        w2 |= (uint32_t)(d2 & 0xFF) << (8 * i);
-      }
-      *(uint32_t*)(d0p + c) = w0;
-      *(uint32_t*)(d0p + C + c) = w1;
-      *(uint32_t*)(d0p + 2 * C + c) = w2;
+    for (int j = 0; j < 4; ++j) {
+      int d0, d1, d2;
+      split_digits((int)rintf(ldexpf(v[j], Ex)), d0, d1, d2);
+      w0 |= (uint32_t)(d0 & 0xFF) << (8 * j);
+      w1 |= (uint32_t)(d1 & 0xFF) << (8 * j);
+      w2 |= (uint32_t)(d2 & 0xFF) << (8 * j);
     }
-    if (lane == 0) xexp[t] = Ex;
+    int8_t* d0p = xdig + (size_t)t * kDigits * C + c;
+    *(uint32_t*)(d0p) = w0;
+    *(uint32_t*)(d0p + C) = w1;
+    *(uint32_t*)(d0p + 2 * C) = w2;
   }
 }
 
@@ -532,15 +733,16 @@ hipError_t launch_decode_prep(const mira_shape& s, const Layout& L, const WsPtr&
   if (L.T == 0) return hipSuccess;
   const int sa = (s.flags & MIRA_FLAG_SOFTMAX_ALL) ? 1 : 0;
   const PermOut o = perm_out(w, counts_out, idx_out, wts_out, offsets_out, order_out);
+  const int max_active = decode_max_active(L);
   prof_begin("decode_prep", st);
   if (s.act_dtype == MIRA_BF16)
     hipLaunchKernelGGL(decode_prep_kernel<uint16_t>, dim3(1), dim3(kBigThreads), 0, st,
                        (const uint16_t*)x, (const uint16_t*)wr, bias, L.T, L.E, L.C, L.k, L.S, sa,
-                       logits_out, ep, o, w.xdig, w.xexp);
+                       logits_out, ep, o, w.dwork, max_active, w.xdig, w.xexp);
   else
     hipLaunchKernelGGL(decode_prep_kernel<float>, dim3(1), dim3(kBigThreads), 0, st,
                        (const float*)x, (const float*)wr, bias, L.T, L.E, L.C, L.k, L.S, sa,
-                       logits_out, ep, o, w.xdig, w.xexp);
+                       logits_out, ep, o, w.dwork, max_active, w.xdig, w.xexp);
   prof_end("decode_prep", st);
   return hipGetLastError();
 }

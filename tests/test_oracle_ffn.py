@@ -36,7 +36,7 @@ def _torch_swiglu(x, wg, wu, wd):
 
 def test_single_expert_is_textbook_swiglu():
     rng = np.random.default_rng(0)
-    C, R, T = 64, 96, 5
+    C, R, T = 64, 128, 5
     wg, wu, wd = _grid_weights(rng, C, R)
     blob = oracle.pack_expert(wg, wu, wd)
     x = rng.standard_normal((T, C))
@@ -50,7 +50,7 @@ def test_single_expert_is_textbook_swiglu():
 
 def test_gate_and_up_roles_are_not_interchangeable():
     rng = np.random.default_rng(1)
-    C, R = 32, 48
+    C, R = 64, 64
     wg, wu, wd = _grid_weights(rng, C, R)
     x = rng.standard_normal((3, C)) * 4
     y = oracle.expert_ffn(oracle.pack_expert(wg, wu, wd), x, C, R)
@@ -60,7 +60,7 @@ def test_gate_and_up_roles_are_not_interchangeable():
 
 def test_zero_input_gives_zero_output():
     rng = np.random.default_rng(2)
-    C, R, E = 32, 64, 4
+    C, R, E = 64, 64, 4
     blobs = [oracle.pack_expert(*_grid_weights(rng, C, R)) for _ in range(E)]
     res = oracle.moe_forward(np.zeros((4, C)), rng.standard_normal((E, C)), rng.standard_normal(E),
                              blobs, 2, C, R)
@@ -69,7 +69,7 @@ def test_zero_input_gives_zero_output():
 
 def test_dense_softmax_moe_when_k_equals_E():
     rng = np.random.default_rng(3)
-    C, R, E, T = 32, 40, 4, 6
+    C, R, E, T = 64, 64, 4, 6
     ws = [_grid_weights(rng, C, R) for _ in range(E)]
     blobs = [oracle.pack_expert(*w) for w in ws]
     x = rng.standard_normal((T, C))
@@ -83,7 +83,7 @@ def test_dense_softmax_moe_when_k_equals_E():
 
 def test_top2_weighted_combine_matches_closed_form():
     rng = np.random.default_rng(4)
-    C, R, E, T = 32, 40, 6, 9
+    C, R, E, T = 64, 64, 6, 9
     ws = [_grid_weights(rng, C, R) for _ in range(E)]
     blobs = [oracle.pack_expert(*w) for w in ws]
     x = rng.standard_normal((T, C))
@@ -99,7 +99,7 @@ def test_top2_weighted_combine_matches_closed_form():
 
 def test_two_shared_experts_equal_one_double_width_expert():
     rng = np.random.default_rng(5)
-    C, R, T = 32, 24, 7
+    C, R, T = 64, 64, 7
     a = _grid_weights(rng, C, R)
     b = _grid_weights(rng, C, R)
     x = rng.standard_normal((T, C))
@@ -120,7 +120,7 @@ def test_two_shared_experts_equal_one_double_width_expert():
 
 def test_relabelling_experts_leaves_output_unchanged():
     rng = np.random.default_rng(6)
-    C, R, E, T, k = 32, 24, 5, 8, 2
+    C, R, E, T, k = 64, 64, 5, 8, 2
     blobs = [oracle.pack_expert(*_grid_weights(rng, C, R)) for _ in range(E)]
     x = rng.standard_normal((T, C))
     wr = rng.standard_normal((E, C))
@@ -133,7 +133,7 @@ def test_relabelling_experts_leaves_output_unchanged():
 
 def test_token_subset_matches_full_rows():
     rng = np.random.default_rng(7)
-    C, R, E, T, k = 32, 24, 4, 10, 2
+    C, R, E, T, k = 64, 64, 4, 10, 2
     blobs = [oracle.pack_expert(*_grid_weights(rng, C, R)) for _ in range(E)]
     x = rng.standard_normal((T, C))
     wr = rng.standard_normal((E, C))

@@ -44,9 +44,22 @@ def _grid_expert(rng, C, R, where_max):
     return (wg, wu, wd), (qg, qu, qd, sigma)
 
 
+def _tiled_bytes(q):
+    """The documented tile layout, element by element: element (r, k) of a
+    [rows][K] matrix goes to tile (r // 16, k // 64), run (k % 64 // 16) * 16 + r % 16,
+    byte k % 16 of the run; tiles are 1024 bytes, row-of-tiles major."""
+    rows, K = q.shape
+    r, k = np.meshgrid(np.arange(rows), np.arange(K), indexing="ij")
+    tile = (r // 16) * (K // 64) + k // 64
+    run = ((k % 64) // 16) * 16 + r % 16
+    off = tile * 1024 + run * 16 + k % 16
+    out = np.empty(rows * K, dtype=np.int8)
+    out[off.reshape(-1)] = q.reshape(-1)
+    return out.view(np.uint8)
+
+
 def _expected_blob(qg, qu, qd, sigma_bits, C, R):
-    raw = np.concatenate([qg.reshape(-1).view(np.uint8), qu.reshape(-1).view(np.uint8),
-                          qd.reshape(-1).view(np.uint8),
+    raw = np.concatenate([_tiled_bytes(qg), _tiled_bytes(qu), _tiled_bytes(qd),
                           np.asarray(sigma_bits, dtype="<u2").view(np.uint8)])
     pad = (-raw.size) % 256
     return np.concatenate([raw, np.zeros(pad, dtype=np.uint8)])
@@ -66,7 +79,7 @@ def test_bf16_rounding_matches_torch():
     assert np.array_equal(oracle.bf16_bits_from_f32(v), _torch_bf16_bits(v))
 
 
-@pytest.mark.parametrize("C,R", [(64, 16), (256, 48), (128, 7)])
+@pytest.mark.parametrize("C,R", [(64, 64), (256, 128), (128, 192)])
 def test_pack_grid_round_trip_bit_exact(C, R):
     rng = np.random.default_rng(C * 1000 + R)
     where = rng.integers(0, 3, size=R)
@@ -79,7 +92,7 @@ def test_pack_grid_round_trip_bit_exact(C, R):
 def test_shared_scale_driven_by_down_column():
     """Rows whose largest magnitude is only in W_down[:, r]: the scale must follow that column."""
     rng = np.random.default_rng(7)
-    C, R = 96, 32
+    C, R = 128, 64
     (wg, wu, wd), (qg, qu, qd, sigma) = _grid_expert(rng, C, R, np.full(R, 2))
     # shrink gate/up so the down column alone carries the maximum
     qg = (qg // 8).astype(np.int8)
@@ -97,21 +110,18 @@ def test_shared_scale_driven_by_down_column():
 def test_pack_ties_golden():
     with open(os.path.join(GOLDEN, "pack_ties.json")) as f:
         g = json.load(f)
-    C, R = g["C"], g["R"]
+    wg, wu, wd, n = _embed_row0(g, "scale_exp2")
     s = np.float32(2.0 ** g["scale_exp2"])
-    wg = (np.float32(g["gate_units"]) * s).reshape(R, C)
-    wu = (np.float32(g["up_units"]) * s).reshape(R, C)
-    wd = (np.float32(g["down_units"]) * s).reshape(C, R)
     blob = oracle.pack_expert(wg, wu, wd)
-    qg, qu, qd, sb = oracle.unpack_expert(blob, C, R)
-    assert qg.reshape(-1).tolist() == g["gate_expected"]
-    assert qu.reshape(-1).tolist() == g["up_expected"]
-    assert qd.reshape(-1).tolist() == g["down_expected"]
+    qg, qu, qd, sb = oracle.unpack_expert(blob, 64, 64)
+    assert qg[0, :n].tolist() == g["gate_expected"]
+    assert qu[0, :n].tolist() == g["up_expected"]
+    assert qd[:n, 0].tolist() == g["down_expected"]
     assert oracle.f32_from_bf16_bits(sb)[0] == s
 
 
 def test_all_zero_row_uses_eps():
-    C, R = 32, 4
+    C, R = 64, 64
     rng = np.random.default_rng(3)
     wg = rng.standard_normal((R, C)).astype(np.float32) * 0.02
     wu = rng.standard_normal((R, C)).astype(np.float32) * 0.02
@@ -130,7 +140,7 @@ def test_all_zero_row_uses_eps():
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_pack_invariants_random(seed):
     rng = np.random.default_rng(seed)
-    C, R = 192, 80
+    C, R = 192, 128
     wg = rng.standard_normal((R, C)).astype(np.float32) * 0.02
     wu = rng.standard_normal((R, C)).astype(np.float32) * 0.02
     wd = (rng.standard_normal((C, R)) * 0.02).astype(np.float32)
@@ -159,7 +169,7 @@ def test_pack_invariants_random(seed):
 
 def test_dequantize_is_scale_times_integer():
     rng = np.random.default_rng(11)
-    C, R = 64, 32
+    C, R = 64, 64
     (wg, wu, wd), _ = _grid_expert(rng, C, R, rng.integers(0, 3, size=R))
     blob = oracle.pack_expert(wg, wu, wd)
     dg, du, dd = oracle.dequantize_expert(blob, C, R)
@@ -176,13 +186,41 @@ def test_pack_rejects_bad_shapes():
 def test_integers_use_the_stored_bf16_scale_golden():
     with open(os.path.join(GOLDEN, "pack_scale_rounding.json")) as f:
         g = json.load(f)
-    C, R = g["C"], g["R"]
-    u = np.float32(2.0 ** g["unit_exp2"])
-    wg = (np.float32(g["gate_units"]) * u).reshape(R, C)
-    wu = (np.float32(g["up_units"]) * u).reshape(R, C)
-    wd = (np.float32(g["down_units"]) * u).reshape(C, R)
-    qg, qu, qd, sb = oracle.unpack_expert(oracle.pack_expert(wg, wu, wd), C, R)
+    wg, wu, wd, n = _embed_row0(g, "unit_exp2")
+    qg, qu, qd, sb = oracle.unpack_expert(oracle.pack_expert(wg, wu, wd), 64, 64)
     assert oracle.f32_from_bf16_bits(sb)[0] == np.float32(2.0 ** g["sigma_expected_exp2"])
-    assert qg.reshape(-1).tolist() == g["gate_expected"]
-    assert qu.reshape(-1).tolist() == g["up_expected"]
-    assert qd.reshape(-1).tolist() == g["down_expected"]
+    assert qg[0, :n].tolist() == g["gate_expected"]
+    assert qu[0, :n].tolist() == g["up_expected"]
+    assert qd[:n, 0].tolist() == g["down_expected"]
+
+
+def _embed_row0(g, exp_key):
+    """Place a golden case's values in row 0 of a 64x64 expert (gate/up row 0,
+    down column 0); every other weight is zero."""
+    u = np.float32(2.0 ** g[exp_key])
+    n = len(g["gate_units"])
+    wg = np.zeros((64, 64), np.float32)
+    wu = np.zeros((64, 64), np.float32)
+    wd = np.zeros((64, 64), np.float32)
+    wg[0, :n] = np.float32(g["gate_units"]) * u
+    wu[0, :n] = np.float32(g["up_units"]) * u
+    wd[:n, 0] = np.float32(g["down_units"]) * u
+    return wg, wu, wd, n
+
+
+def test_tile_layout_golden_offsets():
+    """Hand-computed byte offsets of marked elements in a C=128, R=64 blob."""
+    with open(os.path.join(GOLDEN, "pack_layout.json")) as f:
+        g = json.load(f)
+    C, R = g["C"], g["R"]
+    s = np.float32(2.0 ** -7)
+    mats = {"gate": np.zeros((R, C), np.float32), "up": np.zeros((R, C), np.float32),
+            "down": np.zeros((C, R), np.float32)}
+    for r in range(R):                      # every row needs |q| = 127 somewhere: put it in up
+        mats["up"][r, C - 1] = 127 * s
+    for m in g["marks"]:
+        mats[m["matrix"]][m["row"], m["col"]] = m["q"] * s
+    blob = oracle.pack_expert(mats["gate"], mats["up"], mats["down"])
+    for m in g["marks"]:
+        assert blob.view(np.int8)[m["offset"]] == m["q"], m
+    assert blob[g["sigma_offset"]:g["sigma_offset"] + 2].view("<u2")[0] == 0x3C00  # 2^-7
