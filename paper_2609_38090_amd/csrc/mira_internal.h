@@ -17,7 +17,7 @@ constexpr int kFixBits = 22;         // |fixed-point value| < 2^22
 constexpr int kBlk = 64;             // rows of H' sharing one fixed-point exponent
 constexpr int kTokPerGroup = 5;      // tokens per 16-column MFMA operand (3 digits each)
 constexpr int kDecodeMaxGroups = (MIRA_DECODE_MAX_TOKENS + kTokPerGroup - 1) / kTokPerGroup;
-constexpr int kPrefBM = 64;          // prefill tile: tokens per m-tile (shared by both GEMMs)
+constexpr int kPrefBM = 128;         // prefill tile: tokens per m-tile (shared by both GEMMs)
 
 inline __host__ __device__ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -41,6 +41,7 @@ struct Layout {
   int Pd;       // pairs of the decode sizing
   int Td;       // tokens of the decode sizing
   int mt_max;   // upper bound of prefill m-tiles
+  int ksplit;   // k-chunks of the prefill down GEMM (partials summed in order by the combine)
   size_t logits, idx, wts, counts, offsets, inv, tokpos, wpos, misc, active, mstart, dwork,
       xdig, xexp, hdig, hexp, xb16, hbuf, ybuf, total;
 };
@@ -63,6 +64,13 @@ constexpr int kDecodeMaxPairs = 1024;
 // misc[] slots (int32)
 enum : int { MISC_NACTIVE = 0, MISC_MTOTAL = 1, MISC_COUNT = 16 };
 
+// The prefill down GEMM splits its contraction (R) into this many chunks so
+// that long contractions give the persistent grid enough tiles.
+inline int prefill_ksplit(int R) {
+  const int s = R / 4096;
+  return s < 1 ? 1 : (s > 4 ? 4 : s);
+}
+
 inline int decode_max_active_of(int G, int T, int k, int S) {
   const int pairs_groups = T * k + S;
   return G < pairs_groups ? G : pairs_groups;
@@ -81,6 +89,7 @@ inline Layout make_layout(const mira_shape& s, int T) {
   L.Td = T < MIRA_DECODE_MAX_TOKENS ? T : MIRA_DECODE_MAX_TOKENS;
   L.Pd = L.Td * s.top_k + s.n_shared * L.Td;
   L.mt_max = L.P / kPrefBM + L.G + 1;
+  L.ksplit = prefill_ksplit(s.ffn);
   size_t o = 0;
   auto take = [&](size_t bytes) {
     size_t at = o;
@@ -106,7 +115,7 @@ inline Layout make_layout(const mira_shape& s, int T) {
   L.hexp = take((size_t)L.Pd * (L.R / kBlk) * 4);
   L.xb16 = take(s.act_dtype == MIRA_F32 ? Tz * L.C * 2 : 0);
   L.hbuf = take(P * L.R * 2);
-  L.ybuf = take(P * L.C * 4);
+  L.ybuf = take((size_t)L.ksplit * P * L.C * 4);
   L.total = o;
   return L;
 }
