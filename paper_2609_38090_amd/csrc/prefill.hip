@@ -867,9 +867,10 @@ __global__ __launch_bounds__(kGemmThreads) void prefill_gemm_kernel(
       return Dma{xoff[r], xstage0 + (size_t)s * 128, m0_x + so + r * 1024};
     };
 
-    // the previous tile's stores are done and every wave is done with the
-    // ring before it is refilled
-    wait_vmcnt<0>();
+    // every wave is done with the ring before it is refilled.  The previous
+    // tile's stores may still be in flight: the counter waits below count
+    // only this tile's loads, and as the counter retires in issue order the
+    // older stores only make them stricter.
     ring_barrier();
 
     float* ybase = DUAL ? nullptr : yout + (size_t)t.split * ysplit;
