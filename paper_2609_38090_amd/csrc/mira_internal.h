@@ -42,8 +42,8 @@ struct Layout {
   int Td;       // tokens of the decode sizing
   int mt_max;   // upper bound of prefill m-tiles
   int ksplit;   // k-chunks of the prefill down GEMM (partials summed in order by the combine)
-  size_t logits, idx, wts, counts, offsets, inv, tokpos, wpos, misc, active, mstart, dwork,
-      xdig, xexp, hdig, hexp, xb16, hbuf, ybuf, total;
+  size_t logits, idx, wts, counts, offsets, inv, tokpos, wpos, misc, active, mstart, pcnt,
+      dwork, xdig, xexp, hdig, hexp, xb16, hbuf, ybuf, total;
 };
 
 // One non-empty expert group of a decode call, written by the decode
@@ -60,6 +60,12 @@ struct DecodeWork {
 
 // Largest number of (token, slot) pairs the decode preparation handles.
 constexpr int kDecodeMaxPairs = 1024;
+
+// The prefill permutation runs in chunks of kPermChunk routed pairs, one
+// workgroup each, when there are 2..kPermChunkMax chunks (one workgroup
+// otherwise).
+constexpr int kPermChunk = 1024;
+constexpr int kPermChunkMax = 64;
 
 // misc[] slots (int32)
 enum : int { MISC_NACTIVE = 0, MISC_MTOTAL = 1, MISC_COUNT = 16 };
@@ -108,6 +114,7 @@ inline Layout make_layout(const mira_shape& s, int T) {
   L.misc = take(MISC_COUNT * 4);
   L.active = take(G * 4);
   L.mstart = take((G + 1) * 4);
+  L.pcnt = take((size_t)kPermChunkMax * L.E * 4);
   L.dwork = take(G * sizeof(DecodeWork));
   L.xdig = take((size_t)L.Td * kDigits * L.C);
   L.xexp = take((size_t)L.Td * 4);
@@ -133,6 +140,7 @@ struct WsPtr {
   int32_t* misc;
   int32_t* active;
   int32_t* mstart;
+  int32_t* pcnt;
   DecodeWork* dwork;
   int8_t* xdig;
   int32_t* xexp;
@@ -157,6 +165,7 @@ inline WsPtr ws_ptrs(const Layout& L, void* base) {
   w.misc = (int32_t*)(b + L.misc);
   w.active = (int32_t*)(b + L.active);
   w.mstart = (int32_t*)(b + L.mstart);
+  w.pcnt = (int32_t*)(b + L.pcnt);
   w.dwork = (DecodeWork*)(b + L.dwork);
   w.xdig = (int8_t*)(b + L.xdig);
   w.xexp = (int32_t*)(b + L.xexp);

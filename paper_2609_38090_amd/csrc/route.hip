@@ -15,55 +15,16 @@
 namespace mira {
 
 constexpr int kRouteTok = 16;  // tokens per route workgroup
-constexpr int kRouteThreads = 256;
 constexpr int kBigThreads = 1024;  // permutation and decode-prep workgroups
+static_assert(kPermChunk == kBigThreads, "the chunked permutation runs one thread per pair");
 constexpr int kBigWaves = kBigThreads / 64;
 
 // ---------------------------------------------------------------------------
 // Router logits for 16 tokens: lg[t][e] = sum_c x[t][c] * Wg[e][c] + b[e].
-// bf16: MFMA, A = Wg rows (experts), B = x rows (tokens), fp32 accumulate;
-// waves split the expert tiles.  fp32: VALU dot products, fp32 accumulate.
+// fp32: VALU dot products, one wave per (token, expert), fp32 accumulate.
+// bf16 (below): MFMA, A = Wg rows (experts), B = x rows (tokens), fp32
+// accumulate, the k range split over the waves.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void logits_tile_bf16(const uint16_t* __restrict__ x,
-                                                 const uint16_t* __restrict__ wr,
-                                                 const float* __restrict__ bias, int T, int E,
-                                                 int C, int t0, int nwaves,
-                                                 float (*lg)[MIRA_MAX_EXPERTS]) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r16 = lane & 15, kg = lane >> 4;
-  const int n_et = (E + 15) / 16;
-  const int t = t0 + r16;
-  const bool tok_ok = t < T;
-  const uint16_t* xrow = x + (size_t)(tok_ok ? t : 0) * C + kg * 8;
-  for (int et = wave; et < n_et; et += nwaves) {
-    const int e = et * 16 + r16;
-    const bool e_ok = e < E;
-    const uint16_t* wrow = wr + (size_t)(e_ok ? e : 0) * C + kg * 8;
-    v4f acc = {0.f, 0.f, 0.f, 0.f};
-    int k0 = 0;
-    for (; k0 + 128 <= C; k0 += 128) {
-      v4i a[4], b[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        a[u] = e_ok ? ld16(wrow + k0 + 32 * u) : zero16();
-        b[u] = tok_ok ? ld16(xrow + k0 + 32 * u) : zero16();
-      }
-#pragma unroll
-      for (int u = 0; u < 4; ++u) acc = mfma_bf16(a[u], b[u], acc);
-    }
-    for (; k0 < C; k0 += 32) {
-      v4i a = e_ok ? ld16(wrow + k0) : zero16();
-      v4i b = tok_ok ? ld16(xrow + k0) : zero16();
-      acc = mfma_bf16(a, b, acc);
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {  // D[expert 4*kg+i][token r16]
-      const int ee = et * 16 + kg * 4 + i;
-      if (ee < E) lg[r16][ee] = acc[i] + (bias ? bias[ee] : 0.f);
-    }
-  }
-}
-
 __device__ __forceinline__ void logits_tile_f32(const float* __restrict__ x,
                                                 const float* __restrict__ wr,
                                                 const float* __restrict__ bias, int T, int E,
@@ -82,8 +43,17 @@ __device__ __forceinline__ void logits_tile_f32(const float* __restrict__ x,
   }
 }
 
-// Decode variant for bf16: all waves of the workgroup split the k range of
-// every expert tile; partial sums are reduced through LDS in wave order.
+// Workgroup barrier for LDS traffic only: global loads still in flight (the
+// next expert tile's router rows) are not drained, unlike __syncthreads.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// bf16 logits for up to 16 tokens (decode preparation and prefill routing
+// alike): all waves of the workgroup split the k range of every expert tile;
+// partial sums are reduced through LDS in wave order.
 __device__ __forceinline__ float absmax_bf16x8(v4i v) {
   float m = 0.f;
 #pragma unroll
@@ -94,8 +64,9 @@ __device__ __forceinline__ float absmax_bf16x8(v4i v) {
   return m;
 }
 
-// (also writes max |x[t][:]| of each token into xmax[t]; bias_s is the
-// router bias, staged into LDS by pre_sync() right before the first barrier)
+// x points at the first of T <= 16 tokens.  If xmax is not null it also
+// receives max |x[t][:]| of each token; bias_s is the router bias (or null),
+// staged into LDS by pre_sync() right before the first barrier.
 template <typename PreSync>
 __device__ void logits_ksplit_bf16(const uint16_t* __restrict__ x, const uint16_t* __restrict__ wr,
                                    const float* bias_s, int T, int E, int C,
@@ -107,20 +78,40 @@ __device__ void logits_ksplit_bf16(const uint16_t* __restrict__ x, const uint16_
   const bool tok_ok = r16 < T;
   const uint16_t* xrow = x + (size_t)(tok_ok ? r16 : 0) * C + kg * 8;
   constexpr int B = 8;  // chunks in flight per wave
-  for (int et = 0; et < n_et; ++et) {
+  // When one batch of chunks covers the k range (C <= 4096) the next expert
+  // tile's router rows are loaded while the current tile is reduced.
+  const bool one_batch = nch <= B * kBigWaves;
+  v4i a[B];
+  auto load_rows = [&](int et) {
     const int e = et * 16 + r16;
     const bool e_ok = e < E;
     const uint16_t* wrow = wr + (size_t)(e_ok ? e : 0) * C + kg * 8;
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const int ch = wave + u * kBigWaves;
+      a[u] = (ch < nch && e_ok) ? ld16(wrow + ch * 32) : zero16();
+    }
+  };
+  if (one_batch) load_rows(0);
+  for (int et = 0; et < n_et; ++et) {
     v4f acc = {0.f, 0.f, 0.f, 0.f};
     float xm = 0.f;
     for (int ch0 = wave; ch0 < nch; ch0 += B * kBigWaves) {
-      v4i a[B], b[B];
+      if (!one_batch) {
+        const int e = et * 16 + r16;
+        const bool e_ok = e < E;
+        const uint16_t* wrow = wr + (size_t)(e_ok ? e : 0) * C + kg * 8;
+#pragma unroll
+        for (int u = 0; u < B; ++u) {
+          const int ch = ch0 + u * kBigWaves;
+          a[u] = (ch < nch && e_ok) ? ld16(wrow + ch * 32) : zero16();
+        }
+      }
+      v4i b[B];
 #pragma unroll
       for (int u = 0; u < B; ++u) {
         const int ch = ch0 + u * kBigWaves;
-        const bool in = ch < nch;
-        a[u] = (in && e_ok) ? ld16(wrow + ch * 32) : zero16();
-        b[u] = (in && tok_ok) ? ld16(xrow + ch * 32) : zero16();
+        b[u] = (ch < nch && tok_ok) ? ld16(xrow + ch * 32) : zero16();
       }
 #pragma unroll
       for (int u = 0; u < B; ++u) {
@@ -128,6 +119,7 @@ __device__ void logits_ksplit_bf16(const uint16_t* __restrict__ x, const uint16_
         if (et == 0) xm = fmaxf(xm, absmax_bf16x8(b[u]));
       }
     }
+    if (one_batch && et + 1 < n_et) load_rows(et + 1);
 #pragma unroll
     for (int i = 0; i < 4; ++i) part[wave][r16][kg * 4 + i] = acc[i];  // [token][expert]
     if (et == 0) {
@@ -137,8 +129,8 @@ __device__ void logits_ksplit_bf16(const uint16_t* __restrict__ x, const uint16_
       if (kg == 0) part[wave][r16][16] = xm;  // column 16 is spare
       pre_sync();  // caller's LDS staging, issued before the loads above
     }
-    __syncthreads();
-    if (et == 0 && tid < 16) {
+    lds_barrier();
+    if (et == 0 && xmax && tid < 16) {
       float m = 0.f;
       for (int w = 0; w < kBigWaves; ++w) m = fmaxf(m, part[w][tid][16]);
       xmax[tid] = m;
@@ -149,7 +141,7 @@ __device__ void logits_ksplit_bf16(const uint16_t* __restrict__ x, const uint16_
       for (int w = 0; w < kBigWaves; ++w) s += part[w][tt][ee];
       if (e2 < E) lg[tt][e2] = s + (bias_s ? bias_s[e2] : 0.f);
     }
-    __syncthreads();
+    lds_barrier();
   }
 }
 
@@ -188,31 +180,48 @@ __device__ __forceinline__ void topk_rank(const float* lgrow, int E, int k, int 
   }
 }
 
+// Prefill routing, 16 tokens per workgroup: logits with the k range split
+// over the 16 waves (the same arithmetic as the decode preparation, so both
+// paths route a token identically), then one wave per token for the top-k.
 template <typename ActT>
-__global__ __launch_bounds__(kRouteThreads) void route_kernel(
+__global__ __launch_bounds__(kBigThreads) void route_kernel(
     const ActT* __restrict__ x, const ActT* __restrict__ wr, const float* __restrict__ bias,
     int T, int E, int C, int k, int softmax_all, float* __restrict__ logits_ws,
     float* __restrict__ logits_out, int32_t* __restrict__ idx_ws, float* __restrict__ w_ws) {
   __shared__ float lg[kRouteTok][MIRA_MAX_EXPERTS];
-  __shared__ int sel_e[kRouteThreads / 64][MIRA_MAX_TOPK];
-  __shared__ float sel_v[kRouteThreads / 64][MIRA_MAX_TOPK];
-  const int t0 = blockIdx.x * kRouteTok;
-  if constexpr (sizeof(ActT) == 2)
-    logits_tile_bf16(x, wr, bias, T, E, C, t0, kRouteThreads / 64, lg);
-  else
-    logits_tile_f32(x, wr, bias, T, E, C, t0, kRouteThreads / 64, lg);
-  __syncthreads();
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int tt = wave; tt < kRouteTok; tt += kRouteThreads / 64) {
-    const int t = t0 + tt;
-    if (t >= T) break;
-    for (int e = lane; e < E; e += 64) {
-      logits_ws[(size_t)t * E + e] = lg[tt][e];
-      if (logits_out) logits_out[(size_t)t * E + e] = lg[tt][e];
+  __shared__ float part[kBigWaves][16][17];
+  __shared__ float bias_s[MIRA_MAX_EXPERTS];
+  __shared__ int sel_e[kBigWaves][MIRA_MAX_TOPK];
+  __shared__ float sel_v[kBigWaves][MIRA_MAX_TOPK];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int t0 = blockIdx.x * kRouteTok, nt = min(kRouteTok, T - t0);
+  float bias_r[MIRA_MAX_EXPERTS / kBigThreads + 1];
+#pragma unroll
+  for (int i = 0; i <= MIRA_MAX_EXPERTS / kBigThreads; ++i) {
+    const int e = tid + i * kBigThreads;
+    bias_r[i] = (bias && e < E) ? bias[e] : 0.f;
+  }
+  auto stage = [&]() {
+#pragma unroll
+    for (int i = 0; i <= MIRA_MAX_EXPERTS / kBigThreads; ++i) {
+      const int e = tid + i * kBigThreads;
+      if (e < E) bias_s[e] = bias_r[i];
     }
-    topk_rank(lg[tt], E, k, softmax_all, idx_ws + (size_t)t * k, w_ws + (size_t)t * k, sel_e[wave],
-              sel_v[wave]);
-    __builtin_amdgcn_wave_barrier();  // sel scratch is reused by this wave's next token
+  };
+  if constexpr (sizeof(ActT) == 2) {
+    logits_ksplit_bf16(x + (size_t)t0 * C, wr, bias_s, nt, E, C, part, lg, nullptr, stage);
+  } else {
+    logits_tile_f32(x, wr, bias, T, E, C, t0, kBigWaves, lg);
+    __syncthreads();
+  }
+  if (wave < nt) {
+    const int t = t0 + wave;
+    for (int e = lane; e < E; e += 64) {
+      logits_ws[(size_t)t * E + e] = lg[wave][e];
+      if (logits_out) logits_out[(size_t)t * E + e] = lg[wave][e];
+    }
+    topk_rank(lg[wave], E, k, softmax_all, idx_ws + (size_t)t * k, w_ws + (size_t)t * k,
+              sel_e[wave], sel_v[wave]);
   }
 }
 
@@ -243,19 +252,113 @@ struct PermOut {
   int32_t* order_out;
 };
 
-__device__ void permute_body(const int32_t* idx, const float* wts, int T, int k, int E, int S,
-                             int BM, const ExpertPool& ep, const PermOut& o) {
-  __shared__ int hist[kBigWaves][MIRA_MAX_EXPERTS];
-  __shared__ int off_s[MIRA_MAX_EXPERTS + 1];
+// Group counts and their exclusive scan (wave 0; each lane owns 4
+// consecutive groups): routed group g < E holds count(g) pairs, shared group
+// E + s holds T.  Writes off_s[0..G] in LDS and the counts outputs.
+template <typename CountFn>
+__device__ void group_offsets(CountFn count, int T, int E, int S, int* off_s, const PermOut& o) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, G = E + S;
+  if (wave != 0) return;
+  int c4[4], sum = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int g = lane * 4 + i;
+    const int c = g < E ? count(g) : (g < G ? T : 0);
+    c4[i] = c;
+    sum += c;
+  }
+  int incl = sum;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int v = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += v;
+  }
+  int run = incl - sum;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int g = lane * 4 + i;
+    if (g < G) {
+      off_s[g] = run;
+      o.counts_ws[g] = c4[i];
+      if (o.counts_out) o.counts_out[g] = c4[i];
+    }
+    run += c4[i];
+  }
+  if (lane == 63) off_s[G] = incl;
+}
+
+// Group tables shared by both permutation shapes, from the group offsets
+// off_s[0..G] in LDS: the list of non-empty groups, residency status bits,
+// and the prefill m-tile prefix (tiles of BM positions).  Called by every
+// thread of one workgroup.
+__device__ void group_tables(const int* off_s, int G, int BM, const ExpertPool& ep,
+                             const PermOut& o) {
   __shared__ int mst_s[MIRA_MAX_EXPERTS + 1];
   __shared__ int act_s[MIRA_MAX_EXPERTS];
   __shared__ int n_act_s;
   __shared__ int status_s;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid == 0) status_s = 0;
+  __syncthreads();
+  if (wave == 0) {
+    int cnt4[4], mt4[4], na = 0, nm = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int g = lane * 4 + i;
+      const int c = g < G ? off_s[g + 1] - off_s[g] : 0;
+      cnt4[i] = c;
+      mt4[i] = (c + BM - 1) / BM;
+      na += c > 0;
+      nm += mt4[i];
+    }
+    int ia = na, im = nm;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int va = __shfl_up(ia, off, 64), vm = __shfl_up(im, off, 64);
+      if (lane >= off) {
+        ia += va;
+        im += vm;
+      }
+    }
+    int ra = ia - na, rm = im - nm, bits = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int g = lane * 4 + i;
+      if (g < G) {
+        mst_s[g] = rm;
+        if (cnt4[i] > 0) {
+          act_s[ra++] = g;
+          const int slot = ep.slot_table[g];
+          if (slot < 0) bits |= 1;
+          else if (slot >= ep.n_slots) bits |= 2;
+        }
+      }
+      rm += mt4[i];
+    }
+    if (lane == 63) {
+      n_act_s = ia;
+      mst_s[G] = im;
+    }
+    if (bits) atomicOr(&status_s, bits);
+  }
+  __syncthreads();
+  for (int g = tid; g <= G; g += kBigThreads) o.mstart[g] = mst_s[g];
+  for (int a = tid; a < n_act_s; a += kBigThreads) o.active[a] = act_s[a];
+  if (tid == 0) {
+    o.misc[MISC_NACTIVE] = n_act_s;
+    o.misc[MISC_MTOTAL] = mst_s[G];
+    if (ep.status) *ep.status = status_s;
+  }
+}
+
+__device__ void permute_body(const int32_t* idx, const float* wts, int T, int k, int E, int S,
+                             int BM, const ExpertPool& ep, const PermOut& o) {
+  __shared__ int hist[kBigWaves][MIRA_MAX_EXPERTS];
+  __shared__ int off_s[MIRA_MAX_EXPERTS + 1];
   const int G = E + S, Tk = T * k;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
 
   for (int i = tid; i < kBigWaves * MIRA_MAX_EXPERTS; i += kBigThreads) (&hist[0][0])[i] = 0;
-  if (tid == 0) status_s = 0;
   __syncthreads();
 
   // pass 1: per-wave histograms over contiguous ranges of routed pairs
@@ -269,40 +372,12 @@ __device__ void permute_body(const int32_t* idx, const float* wts, int T, int k,
   }
   __syncthreads();
 
-  // counts and exclusive scan (wave 0: each lane owns 4 consecutive groups)
-  if (wave == 0) {
-    int c4[4], sum = 0;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int g = lane * 4 + i;
-      int c = 0;
-      if (g < E) {
-        for (int w = 0; w < kBigWaves; ++w) c += hist[w][g];
-      } else if (g < G) {
-        c = T;
-      }
-      c4[i] = c;
-      sum += c;
-    }
-    int incl = sum;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int v = __shfl_up(incl, off, 64);
-      if (lane >= off) incl += v;
-    }
-    int run = incl - sum;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int g = lane * 4 + i;
-      if (g < G) {
-        off_s[g] = run;
-        o.counts_ws[g] = c4[i];
-        if (o.counts_out) o.counts_out[g] = c4[i];
-      }
-      run += c4[i];
-    }
-    if (lane == 63) off_s[G] = incl;
-  }
+  // counts and exclusive scan
+  group_offsets([&](int g) {
+    int c = 0;
+    for (int w = 0; w < kBigWaves; ++w) c += hist[w][g];
+    return c;
+  }, T, E, S, off_s, o);
   __syncthreads();
   for (int g = tid; g <= G; g += kBigThreads) {
     o.offsets[g] = off_s[g];
@@ -356,55 +431,103 @@ __device__ void permute_body(const int32_t* idx, const float* wts, int T, int k,
     if (o.order_out) o.order_out[pos] = Tk + i;
   }
 
-  // non-empty groups, residency status, prefill m-tiles
-  if (wave == 0) {
-    int cnt4[4], mt4[4], na = 0, nm = 0;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int g = lane * 4 + i;
-      const int c = g < G ? off_s[g + 1] - off_s[g] : 0;
-      cnt4[i] = c;
-      mt4[i] = (c + BM - 1) / BM;
-      na += c > 0;
-      nm += mt4[i];
-    }
-    int ia = na, im = nm;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int va = __shfl_up(ia, off, 64), vm = __shfl_up(im, off, 64);
-      if (lane >= off) {
-        ia += va;
-        im += vm;
-      }
-    }
-    int ra = ia - na, rm = im - nm, bits = 0;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int g = lane * 4 + i;
-      if (g < G) {
-        mst_s[g] = rm;
-        if (cnt4[i] > 0) {
-          act_s[ra++] = g;
-          const int slot = ep.slot_table[g];
-          if (slot < 0) bits |= 1;
-          else if (slot >= ep.n_slots) bits |= 2;
-        }
-      }
-      rm += mt4[i];
-    }
-    if (lane == 63) {
-      n_act_s = ia;
-      mst_s[G] = im;
-    }
-    if (bits) atomicOr(&status_s, bits);
+  group_tables(off_s, G, BM, ep, o);
+}
+
+// Chunked permutation, first pass: counts of each expert among the routed
+// pairs of chunk blockIdx.x (pcnt[chunk][e]); also copies idx/wts out.
+__global__ __launch_bounds__(kBigThreads) void permute_count_kernel(
+    const int32_t* __restrict__ idx, const float* __restrict__ wts, int Tk, int E,
+    int32_t* __restrict__ pcnt, int32_t* __restrict__ idx_out, float* __restrict__ w_out) {
+  __shared__ int h[MIRA_MAX_EXPERTS];
+  const int tid = threadIdx.x;
+  for (int e = tid; e < E; e += kBigThreads) h[e] = 0;
+  __syncthreads();
+  const int p = blockIdx.x * kPermChunk + tid;
+  if (p < Tk) {
+    const int e = idx[p];
+    atomicAdd(&h[e], 1);
+    if (idx_out) idx_out[p] = e;
+    if (w_out) w_out[p] = wts[p];
   }
   __syncthreads();
-  for (int g = tid; g <= G; g += kBigThreads) o.mstart[g] = mst_s[g];
-  for (int a = tid; a < n_act_s; a += kBigThreads) o.active[a] = act_s[a];
-  if (tid == 0) {
-    o.misc[MISC_NACTIVE] = n_act_s;
-    o.misc[MISC_MTOTAL] = mst_s[G];
-    if (ep.status) *ep.status = status_s;
+  for (int e = tid; e < E; e += kBigThreads) pcnt[blockIdx.x * E + e] = h[e];
+}
+
+// Chunked permutation, second pass (one workgroup per chunk, one thread per
+// pair): the position of a pair is the group offset, plus the pairs of the
+// same expert in earlier chunks, earlier waves of this chunk and earlier
+// lanes of its wave (ballot ranks), so the result equals the one-workgroup
+// permutation.  Each workgroup also places a share of the shared-expert
+// pairs; workgroup 0 writes the group tables.
+__global__ __launch_bounds__(kBigThreads) void permute_scatter_kernel(
+    const int32_t* __restrict__ idx, const float* __restrict__ wts, int T, int k, int E, int S,
+    int BM, int nchunk, const int32_t* __restrict__ pcnt, ExpertPool ep, PermOut o) {
+  __shared__ int hist[kBigWaves][MIRA_MAX_EXPERTS];
+  __shared__ int tot_s[MIRA_MAX_EXPERTS], pre_s[MIRA_MAX_EXPERTS];
+  __shared__ int off_s[MIRA_MAX_EXPERTS + 1];
+  const int G = E + S, Tk = T * k, c = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  for (int e = tid; e < E; e += kBigThreads) {
+    int tot = 0, pre = 0;
+    for (int cc = 0; cc < nchunk; ++cc) {
+      const int v = pcnt[cc * E + e];
+      tot += v;
+      pre += cc < c ? v : 0;
+    }
+    tot_s[e] = tot;
+    pre_s[e] = pre;
+  }
+  // this thread's pair and its rank among the same expert's pairs of the wave
+  const int p = c * kPermChunk + tid;
+  const bool ok = p < Tk;
+  const int e = ok ? idx[p] : 0;
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  uint64_t same = __ballot(ok);
+#pragma unroll
+  for (int bit = 0; bit < 8; ++bit) {
+    const uint64_t b = __ballot(ok && ((e >> bit) & 1));
+    same &= ((e >> bit) & 1) ? b : ~b;
+  }
+  const int rank = __popcll(same & lt_mask);
+  for (int i = tid; i < kBigWaves * MIRA_MAX_EXPERTS; i += kBigThreads) (&hist[0][0])[i] = 0;
+  __syncthreads();
+  if (ok && (same & lt_mask) == 0) hist[wave][e] = __popcll(same);  // one leader per expert
+  group_offsets([&](int g) { return tot_s[g]; }, T, E, S, off_s, o);
+  __syncthreads();
+  // bases of each wave: group offset + earlier chunks + earlier waves
+  for (int g = tid; g < E; g += kBigThreads) {
+    int b = off_s[g] + pre_s[g];
+    for (int w = 0; w < kBigWaves; ++w) {
+      const int n = hist[w][g];
+      hist[w][g] = b;
+      b += n;
+    }
+  }
+  __syncthreads();
+  if (ok) {
+    const int pos = hist[wave][e] + rank;
+    o.inv[p] = pos;
+    o.tokpos[pos] = p / k;
+    o.wpos[pos] = wts[p];
+    if (o.order_out) o.order_out[pos] = p;
+  }
+  // shared experts: every token, in token order, weight 1
+  const int span = (S * T + nchunk - 1) / nchunk;
+  for (int i = c * span + tid; i < min(S * T, (c + 1) * span); i += kBigThreads) {
+    const int s = i / T, t = i - s * T;
+    const int pos = off_s[E + s] + t;
+    o.inv[Tk + i] = pos;
+    o.tokpos[pos] = t;
+    o.wpos[pos] = 1.0f;
+    if (o.order_out) o.order_out[pos] = Tk + i;
+  }
+  if (c == 0) {
+    for (int g = tid; g <= G; g += kBigThreads) {
+      o.offsets[g] = off_s[g];
+      if (o.offsets_out) o.offsets_out[g] = off_s[g];
+    }
+    group_tables(off_s, G, BM, ep, o);
   }
 }
 
@@ -698,7 +821,7 @@ hipError_t launch_route(const mira_shape& s, const Layout& L, const WsPtr& w, co
                         const void* wr, const float* bias, float* logits_out, hipStream_t st) {
   const int T = L.T;
   if (T == 0) return hipSuccess;
-  dim3 grid((T + kRouteTok - 1) / kRouteTok), block(kRouteThreads);
+  dim3 grid((T + kRouteTok - 1) / kRouteTok), block(kBigThreads);
   const int sa = (s.flags & MIRA_FLAG_SOFTMAX_ALL) ? 1 : 0;
   prof_begin("route", st);
   if (s.act_dtype == MIRA_BF16)
@@ -717,10 +840,18 @@ hipError_t launch_permute(const mira_shape& s, const Layout& L, const WsPtr& w,
                           const ExpertPool& ep, int32_t* counts_out, int32_t* idx_out,
                           float* wts_out, int32_t* offsets_out, int32_t* order_out,
                           hipStream_t st) {
+  const PermOut o = perm_out(w, counts_out, idx_out, wts_out, offsets_out, order_out);
+  const int Tk = L.T * L.k, nchunk = (Tk + kPermChunk - 1) / kPermChunk;
   prof_begin("permute", st);
-  hipLaunchKernelGGL(permute_kernel, dim3(1), dim3(kBigThreads), 0, st, w.idx, w.wts, L.T, L.k,
-                     L.E, L.S, kPrefBM, ep,
-                     perm_out(w, counts_out, idx_out, wts_out, offsets_out, order_out));
+  if (nchunk >= 2 && nchunk <= kPermChunkMax) {
+    hipLaunchKernelGGL(permute_count_kernel, dim3(nchunk), dim3(kBigThreads), 0, st, w.idx, w.wts,
+                       Tk, L.E, w.pcnt, idx_out, wts_out);
+    hipLaunchKernelGGL(permute_scatter_kernel, dim3(nchunk), dim3(kBigThreads), 0, st, w.idx,
+                       w.wts, L.T, L.k, L.E, L.S, kPrefBM, nchunk, (const int32_t*)w.pcnt, ep, o);
+  } else {
+    hipLaunchKernelGGL(permute_kernel, dim3(1), dim3(kBigThreads), 0, st, w.idx, w.wts, L.T, L.k,
+                       L.E, L.S, kPrefBM, ep, o);
+  }
   prof_end("permute", st);
   return hipGetLastError();
 }
