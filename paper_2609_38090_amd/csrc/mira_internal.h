@@ -41,7 +41,7 @@ struct Layout {
   int Pd;       // pairs of the decode sizing
   int Td;       // tokens of the decode sizing
   int mt_max;   // upper bound of prefill m-tiles
-  int ksplit;   // k-chunks of the prefill down GEMM (partials summed in order by the combine)
+  int ksplit;   // most k-chunks of the prefill down GEMM (partials summed in order by the combine)
   size_t logits, idx, wts, counts, offsets, inv, tokpos, wpos, misc, active, mstart, pcnt,
       dwork, xdig, xexp, hdig, hexp, xb16, hbuf, ybuf, total;
 };
@@ -68,10 +68,11 @@ constexpr int kPermChunk = 1024;
 constexpr int kPermChunkMax = 64;
 
 // misc[] slots (int32)
-enum : int { MISC_NACTIVE = 0, MISC_MTOTAL = 1, MISC_COUNT = 16 };
+enum : int { MISC_NACTIVE = 0, MISC_MTOTAL = 1, MISC_KSPLIT = 2, MISC_COUNT = 16 };
 
-// The prefill down GEMM splits its contraction (R) into this many chunks so
-// that long contractions give the persistent grid enough tiles.
+// Most k-chunks the prefill down GEMM may split its contraction (R) into
+// (the workspace holds that many fp32 partial outputs); the kernel picks the
+// count that best fills the grid for the actual routing.
 inline int prefill_ksplit(int R) {
   const int s = R / 4096;
   return s < 1 ? 1 : (s > 4 ? 4 : s);

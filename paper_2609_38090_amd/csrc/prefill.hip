@@ -741,8 +741,8 @@ __device__ __forceinline__ void tile_epilogue(const v4f (&acc)[kWaveTiles][MS], 
 
 template <bool DUAL>
 __global__ __launch_bounds__(kGemmThreads) void prefill_gemm_kernel(
-    int C, int R, int G, int KS, ExpertPool ep, const int32_t* __restrict__ misc,
-    const int32_t* __restrict__ mstart, const int32_t* __restrict__ offsets,
+    int C, int R, int G, int KSmax, ExpertPool ep, int32_t* __restrict__ misc,
+    const int32_t* __restrict__ offsets,
     const int32_t* __restrict__ tokpos, const uint16_t* __restrict__ act,
     uint16_t* __restrict__ hout, float* __restrict__ yout, size_t ysplit) {
   // LDS ring of three 48 KB slots: 32 packed tiles exactly as in HBM (1 KB
@@ -756,8 +756,6 @@ __global__ __launch_bounds__(kGemmThreads) void prefill_gemm_kernel(
   const int rows_per_mat = DUAL ? kTileRows / 2 : kTileRows;
   const int NT = (N + rows_per_mat - 1) / rows_per_mat;
   const int nks = K / 64;
-  const int ks_per = (nks + KS - 1) / KS;
-  const int total = misc[MISC_MTOTAL] * NT * KS;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   const int r16 = lane & 15, kg = lane >> 4;
@@ -776,19 +774,62 @@ __global__ __launch_bounds__(kGemmThreads) void prefill_gemm_kernel(
   const uint32_t m0_w = ring_base + wave * kWaveTiles * 1024;
   const uint32_t m0_x = ring_base + kWStage + wave * 32 * 128;
 
-  // group tables in LDS: the tile walk below reads them for every tile
-  __shared__ int32_t s_mstart[MIRA_MAX_EXPERTS + 1], s_off[MIRA_MAX_EXPERTS + 1];
-  __shared__ int32_t s_slot[MIRA_MAX_EXPERTS];
+  // group tables in LDS (offsets, slots and the prefix of m-tiles of kPrefBM
+  // positions over groups); the tile walk below reads them for every tile
+  __shared__ int32_t s_off[MIRA_MAX_EXPERTS + 1], s_slot[MIRA_MAX_EXPERTS];
+  __shared__ int32_t s_mst[MIRA_MAX_EXPERTS + 1];
   for (int i = tid; i <= G; i += kGemmThreads) {
-    s_mstart[i] = mstart[i];
     s_off[i] = offsets[i];
     if (i < G) s_slot[i] = ep.slot_table[i];
   }
   __syncthreads();
+  if (tid < 64) {  // wave 0: each lane owns 4 consecutive groups
+    int m[4], sum = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int g = tid * 4 + i;
+      m[i] = g < G ? (s_off[g + 1] - s_off[g] + kPrefBM - 1) / kPrefBM : 0;
+      sum += m[i];
+    }
+    int incl = sum;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int v = __shfl_up(incl, off, 64);
+      if (tid >= off) incl += v;
+    }
+    int run = incl - sum;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int g = tid * 4 + i;
+      if (g < G) s_mst[g] = run;
+      run += m[i];
+    }
+    if (tid == 63) s_mst[G] = incl;
+  }
+  __syncthreads();
+  // k-chunks: the count (up to KSmax) whose rounds of tiles over the grid
+  // take the fewest stages; ties go to fewer chunks (fewer partials)
+  const int nb = gridDim.x;
+  const int n_mt = s_mst[G];
+  int KS = 1;
+  {
+    long best = -1;
+    for (int ks = 1; ks <= KSmax; ++ks) {
+      const long tiles = (long)n_mt * NT * ks;
+      const long cost = (tiles + nb - 1) / nb * ((nks + ks - 1) / ks);
+      if (best < 0 || cost < best) {
+        best = cost;
+        KS = ks;
+      }
+    }
+  }
+  if (!DUAL && blockIdx.x == 0 && tid == 0) misc[MISC_KSPLIT] = KS;
+  const int ks_per = (nks + KS - 1) / KS;
+  const int per_m = NT * KS;  // tiles per m-tile
+  const int total = n_mt * per_m;
 
   // XCD-aware order: workgroups b, b+8, b+16, ... share an XCD, so give each
   // XCD a contiguous run of logical tiles
-  const int nb = gridDim.x;
   const int bid = (nb % 8 == 0) ? (blockIdx.x % 8) * (nb / 8) + blockIdx.x / 8 : blockIdx.x;
 
   // tile tau -> (group, m-tile, k-chunk, n-tile): groups in order, m-tiles
@@ -800,11 +841,11 @@ __global__ __launch_bounds__(kGemmThreads) void prefill_gemm_kernel(
     int g = 0, hi = G;
     while (hi - g > 1) {
       const int mid = (g + hi) >> 1;
-      if (s_mstart[mid] * NT * KS <= tau) g = mid;
+      if (s_mst[mid] * per_m <= tau) g = mid;
       else hi = mid;
     }
-    const int mt_g = s_mstart[g + 1] - s_mstart[g];
-    const int local = tau - s_mstart[g] * NT * KS;
+    const int mt_g = s_mst[g + 1] - s_mst[g];
+    const int local = tau - s_mst[g] * per_m;
     const int ml = local % mt_g, rest = local / mt_g;
     const int p0 = s_off[g] + ml * kPrefBM;
     return Tile{g, p0, min(kPrefBM, s_off[g + 1] - p0), rest % KS, (rest / KS) * rows_per_mat};
@@ -893,8 +934,10 @@ __global__ __launch_bounds__(kGemmThreads) void prefill_gemm_kernel(
 }
 
 // out[t][c] = sum_j w[t][j] * Y[inv[t*k+j]][c] + sum_s Y[inv[T*k + s*T + t]][c],
-// each Y the ordered sum of its KS k-chunk partials
-__global__ __launch_bounds__(256) void combine_kernel(int T, int C, int k, int S, int KS,
+// each Y the ordered sum of its KS k-chunk partials (KS chosen by the down
+// GEMM and read from misc)
+__global__ __launch_bounds__(256) void combine_kernel(int T, int C, int k, int S,
+                                                      const int32_t* __restrict__ misc,
                                                       size_t ysplit,
                                                       const int32_t* __restrict__ inv,
                                                       const float* __restrict__ wts,
@@ -903,6 +946,7 @@ __global__ __launch_bounds__(256) void combine_kernel(int T, int C, int k, int S
   const int t = blockIdx.y;
   const int c = (blockIdx.x * 256 + threadIdx.x) * 4;
   if (c >= C) return;
+  const int KS = misc[MISC_KSPLIT];
   auto yrow = [&](size_t pos) {
     v4f v = *(const v4f*)(y + pos * C + c);
     for (int sp = 1; sp < KS; ++sp) v += *(const v4f*)(y + sp * ysplit + pos * C + c);
@@ -956,7 +1000,7 @@ hipError_t launch_prefill(const mira_shape& s, const Layout& L, const WsPtr& w, 
     const int grid = persistent_grid(kern, occ, tiles);
     prof_begin("prefill_gateup", st);
     hipLaunchKernelGGL(kern, dim3(grid), dim3(kGemmThreads), 0, st, L.C, L.R, L.G, 1, ep, w.misc,
-                       w.mstart, w.offsets, w.tokpos, xb, w.hbuf, (float*)nullptr, (size_t)0);
+                       w.offsets, w.tokpos, xb, w.hbuf, (float*)nullptr, (size_t)0);
     prof_end("prefill_gateup", st);
   }
   {
@@ -966,15 +1010,15 @@ hipError_t launch_prefill(const mira_shape& s, const Layout& L, const WsPtr& w, 
     const int grid = persistent_grid(kern, occ, tiles);
     prof_begin("prefill_down", st);
     hipLaunchKernelGGL(kern, dim3(grid), dim3(kGemmThreads), 0, st, L.C, L.R, L.G, L.ksplit, ep,
-                       w.misc, w.mstart, w.offsets, w.tokpos, (const uint16_t*)w.hbuf,
+                       w.misc, w.offsets, w.tokpos, (const uint16_t*)w.hbuf,
                        (uint16_t*)nullptr, w.ybuf, ysplit);
     prof_end("prefill_down", st);
   }
   {
     dim3 grid((L.C / 4 + 255) / 256, T);
     prof_begin("prefill_combine", st);
-    hipLaunchKernelGGL(combine_kernel, grid, dim3(256), 0, st, T, L.C, L.k, L.S, L.ksplit, ysplit,
-                       w.inv, w.wts, w.ybuf, out);
+    hipLaunchKernelGGL(combine_kernel, grid, dim3(256), 0, st, T, L.C, L.k, L.S,
+                       (const int32_t*)w.misc, ysplit, w.inv, w.wts, w.ybuf, out);
     prof_end("prefill_combine", st);
   }
   return hipGetLastError();
