@@ -279,14 +279,10 @@ static void launch_decode_ffn(const Layout& L, const WsPtr& w, const ExpertPool&
                               hipStream_t st) {
   const int nrb = L.R / kBlk;
   const int max_active = decode_max_active(L);
-  prof_begin("decode_gateup", st);
-  hipLaunchKernelGGL(decode_gateup_kernel<NG>, dim3(max_active * nrb), dim3(256), 0, st, L.C, L.R,
-                     ep, w.dwork, w.xdig, w.hdig, w.hexp);
-  prof_end("decode_gateup", st);
-  prof_begin("decode_down", st);
-  hipLaunchKernelGGL((decode_down_kernel<NG, kDownKS>), dim3(L.C / 16), dim3(64 * kDownKS), 0, st,
-                     L.C, L.R, L.T, max_active, ep, w.dwork, w.hdig, w.hexp, out);
-  prof_end("decode_down", st);
+  launch_timed("decode_gateup", decode_gateup_kernel<NG>, dim3(max_active * nrb), dim3(256), 0, st,
+               L.C, L.R, ep, w.dwork, w.xdig, w.hdig, w.hexp);
+  launch_timed("decode_down", (decode_down_kernel<NG, kDownKS>), dim3(L.C / 16), dim3(64 * kDownKS),
+               0, st, L.C, L.R, L.T, max_active, ep, w.dwork, w.hdig, w.hexp, out);
 }
 
 hipError_t launch_decode(const mira_shape& s, const Layout& L, const WsPtr& w, const void* x,

@@ -286,6 +286,17 @@ void prof_begin(const char* name, hipStream_t st) {
   g_prof.push_back(r);
 }
 
+void prof_events(const char* name, hipEvent_t* start, hipEvent_t* stop) {
+  *start = *stop = nullptr;
+  std::lock_guard<std::mutex> g(g_prof_mu);
+  if (!g_prof_on) return;
+  if (!g_prof_only.empty() && g_prof_only != name) return;
+  ProfRec r{name, prof_event(), prof_event()};
+  if (!r.a || !r.b) return;
+  *start = r.a;
+  *stop = r.b;
+  g_prof.push_back(r);
+}
 void prof_end(const char* name, hipStream_t st) {
   std::lock_guard<std::mutex> g(g_prof_mu);
   if (!g_prof_on) return;

@@ -2,6 +2,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stddef.h>
 #include <stdint.h>
 
@@ -195,6 +196,18 @@ struct ExpertPool {
 // Kernel timing hooks (mira_api.cpp); no-ops unless profiling is enabled.
 void prof_begin(const char* name, hipStream_t st);
 void prof_end(const char* name, hipStream_t st);
+// Events for one timed launch of kernel `name` (both null unless profiling
+// selects it); the dispatch packet itself records them, so the interval is
+// the kernel's own start and end.
+void prof_events(const char* name, hipEvent_t* start, hipEvent_t* stop);
+
+template <typename... Args, typename F = void (*)(Args...)>
+inline void launch_timed(const char* name, F kernel, dim3 grid, dim3 block, uint32_t shmem,
+                         hipStream_t st, Args... args) {
+  hipEvent_t a = nullptr, b = nullptr;
+  prof_events(name, &a, &b);
+  hipExtLaunchKernelGGL(kernel, grid, block, shmem, st, a, b, 0, args...);
+}
 
 hipError_t launch_route(const mira_shape& s, const Layout& L, const WsPtr& w, const void* x,
                         const void* wr, const float* bias, float* logits_out, hipStream_t st);

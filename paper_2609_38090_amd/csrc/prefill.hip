@@ -986,10 +986,8 @@ hipError_t launch_prefill(const mira_shape& s, const Layout& L, const WsPtr& w, 
   if (s.act_dtype == MIRA_F32) {
     const size_t n = (size_t)T * L.C;
     const int blocks = (int)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096);
-    prof_begin("prefill_cvt", st);
-    hipLaunchKernelGGL(f32_to_bf16_kernel, dim3(blocks), dim3(256), 0, st, (const float*)x,
-                       w.xb16, n);
-    prof_end("prefill_cvt", st);
+    launch_timed("prefill_cvt", f32_to_bf16_kernel, dim3(blocks), dim3(256), 0, st, (const float*)x,
+                 w.xb16, n);
     xb = w.xb16;
   }
   const size_t ysplit = (size_t)L.P * L.C;
@@ -998,28 +996,22 @@ hipError_t launch_prefill(const mira_shape& s, const Layout& L, const WsPtr& w, 
     static int occ = 0;
     const long tiles = (long)L.mt_max * ((L.R + kTileRows / 2 - 1) / (kTileRows / 2));
     const int grid = persistent_grid(kern, occ, tiles);
-    prof_begin("prefill_gateup", st);
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(kGemmThreads), 0, st, L.C, L.R, L.G, 1, ep, w.misc,
-                       w.offsets, w.tokpos, xb, w.hbuf, (float*)nullptr, (size_t)0);
-    prof_end("prefill_gateup", st);
+    launch_timed("prefill_gateup", kern, dim3(grid), dim3(kGemmThreads), 0, st, L.C, L.R, L.G, 1,
+                 ep, w.misc, w.offsets, w.tokpos, xb, w.hbuf, (float*)nullptr, (size_t)0);
   }
   {
     auto kern = prefill_gemm_kernel<false>;
     static int occ = 0;
     const long tiles = (long)L.mt_max * ((L.C + kTileRows - 1) / kTileRows) * L.ksplit;
     const int grid = persistent_grid(kern, occ, tiles);
-    prof_begin("prefill_down", st);
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(kGemmThreads), 0, st, L.C, L.R, L.G, L.ksplit, ep,
-                       w.misc, w.offsets, w.tokpos, (const uint16_t*)w.hbuf,
-                       (uint16_t*)nullptr, w.ybuf, ysplit);
-    prof_end("prefill_down", st);
+    launch_timed("prefill_down", kern, dim3(grid), dim3(kGemmThreads), 0, st, L.C, L.R, L.G,
+                 L.ksplit, ep, w.misc, w.offsets, w.tokpos, (const uint16_t*)w.hbuf,
+                 (uint16_t*)nullptr, w.ybuf, ysplit);
   }
   {
     dim3 grid((L.C / 4 + 255) / 256, T);
-    prof_begin("prefill_combine", st);
-    hipLaunchKernelGGL(combine_kernel, grid, dim3(256), 0, st, T, L.C, L.k, L.S,
-                       (const int32_t*)w.misc, ysplit, w.inv, w.wts, w.ybuf, out);
-    prof_end("prefill_combine", st);
+    launch_timed("prefill_combine", combine_kernel, grid, dim3(256), 0, st, T, L.C, L.k, L.S,
+                 (const int32_t*)w.misc, ysplit, w.inv, w.wts, w.ybuf, out);
   }
   return hipGetLastError();
 }
