@@ -1,0 +1,446 @@
+// Device-side routing helpers shared by the routing kernels and the fused
+// decode kernel: router logits for up to 16 tokens, top-k by rank counting
+// with the combine weights, and the one-wave stable grouping of a decode
+// call's (token, slot) pairs (paper section II-A: the router scores every
+// expert, the top-k experts process the token, their outputs are combined).
+#pragma once
+
+#include "device_util.h"
+#include "mira_internal.h"
+
+namespace mira {
+
+constexpr int kRouteTok = 16;  // tokens per route workgroup
+constexpr int kBigThreads = 1024;  // permutation and decode-prep workgroups
+static_assert(kPermChunk == kBigThreads, "the chunked permutation runs one thread per pair");
+constexpr int kBigWaves = kBigThreads / 64;
+
+// ---------------------------------------------------------------------------
+// Router logits for 16 tokens: lg[t][e] = sum_c x[t][c] * Wg[e][c] + b[e].
+// fp32: VALU dot products, one wave per (token, expert), fp32 accumulate.
+// bf16 (below): MFMA, A = Wg rows (experts), B = x rows (tokens), fp32
+// accumulate, the k range split over the waves.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void logits_tile_f32(const float* __restrict__ x,
+                                                const float* __restrict__ wr,
+                                                const float* __restrict__ bias, int T, int E,
+                                                int C, int t0, int nwaves,
+                                                float (*lg)[MIRA_MAX_EXPERTS]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int ntok = min(kRouteTok, T - t0);
+  for (int pr = wave; pr < ntok * E; pr += nwaves) {
+    const int tt = pr / E, e = pr - tt * E;
+    const float* xr = x + (size_t)(t0 + tt) * C;
+    const float* wrow = wr + (size_t)e * C;
+    float s = 0.f;
+    for (int c = lane; c < C; c += 64) s = fmaf(xr[c], wrow[c], s);
+    s = wave_sum(s);
+    if (lane == 0) lg[tt][e] = s + (bias ? bias[e] : 0.f);
+  }
+}
+
+// Workgroup barrier for LDS traffic only: global loads still in flight (the
+// next expert tile's router rows) are not drained, unlike __syncthreads.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// bf16 logits for up to 16 tokens (decode preparation and prefill routing
+// alike): all waves of the workgroup split the k range of every expert tile;
+// partial sums are reduced through LDS in wave order.
+__device__ __forceinline__ float absmax_bf16x8(v4i v) {
+  float m = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t u = (uint32_t)v[i];
+    m = fmaxf(m, fmaxf(fabsf(__uint_as_float(u << 16)), fabsf(__uint_as_float(u & 0xFFFF0000u))));
+  }
+  return m;
+}
+
+// x points at the first of T <= 16 tokens.  If xmax is not null it also
+// receives max |x[t][:]| of each token; bias_s is the router bias (or null),
+// staged into LDS by pre_sync() right before the first barrier.
+template <typename PreSync>
+__device__ void logits_ksplit_bf16(const uint16_t* __restrict__ x, const uint16_t* __restrict__ wr,
+                                   const float* bias_s, int T, int E, int C,
+                                   float (*part)[16][17], float (*lg)[MIRA_MAX_EXPERTS],
+                                   float* xmax, PreSync pre_sync) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, kg = lane >> 4;
+  const int n_et = (E + 15) / 16, nch = C / 32;
+  const bool tok_ok = r16 < T;
+  const uint16_t* xrow = x + (size_t)(tok_ok ? r16 : 0) * C + kg * 8;
+  constexpr int B = 8;  // chunks in flight per wave
+  // When one batch of chunks covers the k range (C <= 4096) the next expert
+  // tile's router rows are loaded while the current tile is reduced.
+  const bool one_batch = nch <= B * kBigWaves;
+  v4i a[B];
+  auto load_rows = [&](int et) {
+    const int e = et * 16 + r16;
+    const bool e_ok = e < E;
+    const uint16_t* wrow = wr + (size_t)(e_ok ? e : 0) * C + kg * 8;
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const int ch = wave + u * kBigWaves;
+      a[u] = (ch < nch && e_ok) ? ld16(wrow + ch * 32) : zero16();
+    }
+  };
+  if (one_batch) load_rows(0);
+  for (int et = 0; et < n_et; ++et) {
+    v4f acc = {0.f, 0.f, 0.f, 0.f};
+    float xm = 0.f;
+    for (int ch0 = wave; ch0 < nch; ch0 += B * kBigWaves) {
+      if (!one_batch) {
+        const int e = et * 16 + r16;
+        const bool e_ok = e < E;
+        const uint16_t* wrow = wr + (size_t)(e_ok ? e : 0) * C + kg * 8;
+#pragma unroll
+        for (int u = 0; u < B; ++u) {
+          const int ch = ch0 + u * kBigWaves;
+          a[u] = (ch < nch && e_ok) ? ld16(wrow + ch * 32) : zero16();
+        }
+      }
+      v4i b[B];
+#pragma unroll
+      for (int u = 0; u < B; ++u) {
+        const int ch = ch0 + u * kBigWaves;
+        b[u] = (ch < nch && tok_ok) ? ld16(xrow + ch * 32) : zero16();
+      }
+#pragma unroll
+      for (int u = 0; u < B; ++u) {
+        acc = mfma_bf16(a[u], b[u], acc);
+        if (et == 0) xm = fmaxf(xm, absmax_bf16x8(b[u]));
+      }
+    }
+    if (one_batch && et + 1 < n_et) load_rows(et + 1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) part[wave][r16][kg * 4 + i] = acc[i];  // [token][expert]
+    if (et == 0) {
+      // this wave's max over its chunks of token r16: combine the 4 lane groups
+      xm = fmaxf(xm, __shfl_xor(xm, 16, 64));
+      xm = fmaxf(xm, __shfl_xor(xm, 32, 64));
+      if (kg == 0) part[wave][r16][16] = xm;  // column 16 is spare
+      pre_sync();  // caller's LDS staging, issued before the loads above
+    }
+    lds_barrier();
+    if (et == 0 && xmax && tid < 16) {
+      float m = 0.f;
+      for (int w = 0; w < kBigWaves; ++w) m = fmaxf(m, part[w][tid][16]);
+      xmax[tid] = m;
+    }
+    if (tid < 256) {
+      const int tt = tid >> 4, ee = tid & 15, e2 = et * 16 + ee;
+      float s = 0.f;
+      for (int w = 0; w < kBigWaves; ++w) s += part[w][tt][ee];
+      if (e2 < E) lg[tt][e2] = s + (bias_s ? bias_s[e2] : 0.f);
+    }
+    lds_barrier();
+  }
+}
+
+// The logits of logits_ksplit_bf16 from a workgroup of NW < 16 waves: wave w
+// computes the partial sums of k-range slices w*16/NW .. (w+1)*16/NW - 1, each
+// with the chunk order and MFMA chain of one wave of the 16-wave split, and
+// the 16 partials are reduced in slice order, so both shapes give
+// bit-identical logits (and the same max |x| per token).  bias_s must be in
+// LDS before the call; only rows t < T of lg are written, xmax needs 16 entries.
+template <int NW>
+__device__ void logits_slices_bf16(const uint16_t* __restrict__ x, const uint16_t* __restrict__ wr,
+                                   const float* bias_s, int T, int E, int C,
+                                   float (*part)[16][17], float (*lg)[MIRA_MAX_EXPERTS],
+                                   float* xmax) {
+  static_assert(kBigWaves % NW == 0, "slices per wave");
+  constexpr int VPW = kBigWaves / NW;
+  constexpr int B = 8;  // chunks per batch, as in the 16-wave split
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, kg = lane >> 4;
+  const int n_et = (E + 15) / 16, nch = C / 32;
+  const bool tok_ok = r16 < T;
+  const uint16_t* xrow = x + (size_t)(tok_ok ? r16 : 0) * C + kg * 8;
+  for (int et = 0; et < n_et; ++et) {
+    const int e = et * 16 + r16;
+    const bool e_ok = e < E;
+    const uint16_t* wrow = wr + (size_t)(e_ok ? e : 0) * C + kg * 8;
+    for (int j = 0; j < VPW; ++j) {
+      const int vw = wave * VPW + j;
+      v4f acc = {0.f, 0.f, 0.f, 0.f};
+      float xm = 0.f;
+      for (int ch0 = vw; ch0 < nch; ch0 += B * kBigWaves) {
+        v4i a[B], b[B];
+#pragma unroll
+        for (int u = 0; u < B; ++u) {
+          const int ch = ch0 + u * kBigWaves;
+          a[u] = (ch < nch && e_ok) ? ld16(wrow + ch * 32) : zero16();
+          b[u] = (ch < nch && tok_ok) ? ld16(xrow + ch * 32) : zero16();
+        }
+#pragma unroll
+        for (int u = 0; u < B; ++u) {
+          acc = mfma_bf16(a[u], b[u], acc);
+          if (et == 0) xm = fmaxf(xm, absmax_bf16x8(b[u]));
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) part[vw][r16][kg * 4 + i] = acc[i];  // [token][expert]
+      if (et == 0) {
+        xm = fmaxf(xm, __shfl_xor(xm, 16, 64));
+        xm = fmaxf(xm, __shfl_xor(xm, 32, 64));
+        if (kg == 0) part[vw][r16][16] = xm;
+      }
+    }
+    __syncthreads();
+    if (et == 0 && xmax && tid < 16) {
+      float m = 0.f;
+      for (int w = 0; w < kBigWaves; ++w) m = fmaxf(m, part[w][tid][16]);
+      xmax[tid] = m;
+    }
+    for (int i = tid; i < 256; i += NW * 64) {
+      const int tt = i >> 4, ee = i & 15, e2 = et * 16 + ee;
+      float sum = 0.f;
+      for (int w = 0; w < kBigWaves; ++w) sum += part[w][tt][ee];
+      if (e2 < E && tt < T) lg[tt][e2] = sum + (bias_s ? bias_s[e2] : 0.f);
+    }
+    __syncthreads();
+  }
+}
+
+// Top-k of one token by rank counting (one wave): expert e is selected at
+// position rank(e) = number of experts with a larger (value, then lower
+// index) key, if that is < k.  Every lane reads the logits by LDS broadcast,
+// so no cross-lane shuffles are needed.  sel_e/sel_v: this wave's LDS scratch.
+__device__ __forceinline__ void topk_rank(const float* lgrow, int E, int k, int softmax_all,
+                                          int32_t* idx_a, float* w_a, int* sel_e, float* sel_v) {
+  const int lane = threadIdx.x & 63;
+  for (int e = lane; e < E; e += 64) {
+    const uint32_t ke = f32_order_key(lgrow[e]);
+    int rank = 0;
+    for (int e2 = 0; e2 < E; ++e2) {
+      const uint32_t k2 = f32_order_key(lgrow[e2]);
+      rank += (k2 > ke) || (k2 == ke && e2 < e);
+    }
+    if (rank < k) {
+      sel_e[rank] = e;
+      sel_v[rank] = lgrow[e];
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
+  const float vmax = sel_v[0];
+  float denom = 0.f;
+  if (softmax_all) {
+    float s = 0.f;
+    for (int e = lane; e < E; e += 64) s += expf(lgrow[e] - vmax);
+    denom = wave_sum(s);
+  } else {
+    for (int j = 0; j < k; ++j) denom += expf(sel_v[j] - vmax);
+  }
+  if (lane < k) {
+    idx_a[lane] = sel_e[lane];
+    w_a[lane] = expf(sel_v[lane] - vmax) / denom;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Stable grouping of (token, slot) pairs by expert (one 1024-thread
+// workgroup).  Routed pair p = t*k + j goes to expert idx[p]; shared expert s
+// owns pairs T*k + s*T + t.  Groups: routed experts 0..E-1 then shared
+// 0..S-1; inside a group pairs keep increasing p.  Outputs: counts, offsets,
+// inv[p] = position, tokpos/wpos (token and combine weight at each position),
+// the list of non-empty groups, the prefill m-tile prefix, and residency
+// status bits.  Ranks come from wave ballots, never from the order of
+// atomics, so the result is deterministic.  idx and wts may point to LDS or
+// global memory.
+// ---------------------------------------------------------------------------
+struct PermOut {
+  int32_t* counts_ws;
+  int32_t* offsets;
+  int32_t* inv;
+  int32_t* tokpos;
+  float* wpos;
+  int32_t* misc;
+  int32_t* active;
+  int32_t* mstart;
+  int32_t* counts_out;
+  int32_t* idx_out;
+  float* w_out;
+  int32_t* offsets_out;
+  int32_t* order_out;
+};
+
+// ---------------------------------------------------------------------------
+// Stable grouping for a decode call (T <= 16 tokens, at most kDecodeMaxPairs
+// pairs) by one wave: chunks of 64 pairs in order, ranks from ballots, running
+// group bases in LDS.  Same outputs as permute_body, plus one DecodeWork
+// descriptor per non-empty group.
+// ---------------------------------------------------------------------------
+__device__ inline void permute_decode_wave(const int32_t* idx, const float* wts, const int* xe_s,
+                                           const int* slot_s, int T, int k, int E, int S,
+                                           const ExpertPool& ep, const PermOut& o,
+                                           DecodeWork* __restrict__ work, int max_active,
+                                           int* cnt_s, int* run_s, int* ptok_s, float* pw_s) {
+  // reused once the counts and running bases are consumed: per non-empty group
+  int* act_off_s = cnt_s;
+  int* act_n_s = run_s;
+  const int lane = threadIdx.x & 63;
+  const int G = E + S, Tk = T * k;
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int g = lane; g < G; g += 64) cnt_s[g] = g >= E ? T : 0;
+  __builtin_amdgcn_wave_barrier();
+  auto match = [&](bool ok, int e) {
+    uint64_t same = __ballot(ok);
+#pragma unroll
+    for (int bit = 0; bit < 8; ++bit) {
+      const uint64_t bb = __ballot(ok && ((e >> bit) & 1));
+      same &= ((e >> bit) & 1) ? bb : ~bb;
+    }
+    return same;
+  };
+  for (int base = 0; base < Tk; base += 64) {
+    const int p = base + lane;
+    const bool ok = p < Tk;
+    const int e = ok ? idx[p] : 0;
+    const uint64_t same = match(ok, e);
+    if (ok && (same & lt_mask) == 0) cnt_s[e] += __popcll(same);
+    __builtin_amdgcn_wave_barrier();
+    if (ok) {
+      if (o.idx_out) o.idx_out[p] = e;
+      if (o.w_out) o.w_out[p] = wts[p];
+    }
+  }
+  // one exclusive scan over groups (4 consecutive groups per lane) carrying
+  // both the pair count (low 16 bits) and the non-empty group count (high)
+  int c4[4], sum = 0, nz = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int g = lane * 4 + i;
+    c4[i] = g < G ? cnt_s[g] : 0;
+    sum += c4[i];
+    nz += c4[i] > 0;
+  }
+  int packed = sum | (nz << 16);
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int v = __shfl_up(packed, off, 64);
+    if (lane >= off) packed += v;
+  }
+  const int incl = packed & 0xFFFF, ia = packed >> 16, na = nz;
+  int run = incl - sum;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int g = lane * 4 + i;
+    if (g < G) {
+      run_s[g] = run;
+      o.counts_ws[g] = c4[i];
+      o.offsets[g] = run;
+      if (o.counts_out) o.counts_out[g] = c4[i];
+      if (o.offsets_out) o.offsets_out[g] = run;
+    }
+    run += c4[i];
+  }
+  if (lane == 63) {
+    o.offsets[G] = incl;
+    if (o.offsets_out) o.offsets_out[G] = incl;
+  }
+  __builtin_amdgcn_wave_barrier();
+  // positions of routed pairs
+  for (int base = 0; base < Tk; base += 64) {
+    const int p = base + lane;
+    const bool ok = p < Tk;
+    const int e = ok ? idx[p] : 0;
+    const uint64_t same = match(ok, e);
+    int b0 = 0;
+    if (ok) b0 = run_s[e];
+    __builtin_amdgcn_wave_barrier();  // every lane has read its base
+    if (ok) {
+      const int pos = b0 + __popcll(same & lt_mask);
+      const float w = wts[p];
+      o.inv[p] = pos;
+      o.tokpos[pos] = p / k;
+      o.wpos[pos] = w;
+      ptok_s[pos] = p / k;
+      pw_s[pos] = w;
+      if (o.order_out) o.order_out[pos] = p;
+      if ((same & lt_mask) == 0) run_s[e] = b0 + __popcll(same);
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+  // shared experts: every token in order, weight 1 (their bases were not advanced)
+  for (int i = lane; i < S * T; i += 64) {
+    const int s = i / T, t = i - s * T;
+    const int pos = run_s[E + s] + t;
+    o.inv[Tk + i] = pos;
+    o.tokpos[pos] = t;
+    o.wpos[pos] = 1.0f;
+    ptok_s[pos] = t;
+    pw_s[pos] = 1.0f;
+    if (o.order_out) o.order_out[pos] = Tk + i;
+  }
+  __builtin_amdgcn_wave_barrier();
+  // non-empty groups in order -> descriptors (headers by the owning lane,
+  // then the per-position fields spread over all lanes)
+  const int n_active = __shfl(ia, 63, 64);
+  int ra = ia - na, bits = 0;
+  int gbase = incl - sum;
+  for (int i = 0; i < 4; ++i) {
+    const int g = lane * 4 + i;
+    if (g < G && c4[i] > 0) {
+      const int slot = slot_s[g];
+      if (slot < 0) bits |= 1;
+      else if (slot >= ep.n_slots) bits |= 2;
+      o.active[ra] = g;
+      DecodeWork* wk = work + ra;
+      wk->group = g;
+      wk->slot = slot;
+      wk->off = gbase;
+      wk->n = c4[i];
+      act_off_s[ra] = gbase;
+      act_n_s[ra] = c4[i];
+      ++ra;
+    }
+    gbase += c4[i];
+  }
+  __builtin_amdgcn_wave_barrier();
+  for (int it = lane; it < n_active * MIRA_DECODE_MAX_TOKENS; it += 64) {
+    const int a = it / MIRA_DECODE_MAX_TOKENS, j = it - a * MIRA_DECODE_MAX_TOKENS;
+    const int off = act_off_s[a];
+    const bool v = j < act_n_s[a];
+    const int t = v ? ptok_s[off + j] : 0;
+    work[a].tok[j] = t;
+    work[a].xe[j] = v ? xe_s[t] : 0;
+    work[a].w[j] = v ? pw_s[off + j] : 0.f;
+  }
+  for (int a = n_active + lane; a < max_active; a += 64) work[a].group = -1;
+  bits |= __shfl_xor(bits, 1, 64);
+  bits |= __shfl_xor(bits, 2, 64);
+  bits |= __shfl_xor(bits, 4, 64);
+  bits |= __shfl_xor(bits, 8, 64);
+  bits |= __shfl_xor(bits, 16, 64);
+  bits |= __shfl_xor(bits, 32, 64);
+  if (lane == 0) {
+    o.misc[MISC_NACTIVE] = n_active;
+    o.misc[MISC_MTOTAL] = 0;
+    if (ep.status) *ep.status = bits;
+  }
+}
+
+inline PermOut perm_out(const WsPtr& w, int32_t* counts_out, int32_t* idx_out, float* wts_out,
+                        int32_t* offsets_out, int32_t* order_out) {
+  PermOut o;
+  o.counts_ws = w.counts;
+  o.offsets = w.offsets;
+  o.inv = w.inv;
+  o.tokpos = w.tokpos;
+  o.wpos = w.wpos;
+  o.misc = w.misc;
+  o.active = w.active;
+  o.mstart = w.mstart;
+  o.counts_out = counts_out;
+  o.idx_out = idx_out;
+  o.w_out = wts_out;
+  o.offsets_out = offsets_out;
+  o.order_out = order_out;
+  return o;
+}
+
+}  // namespace mira
