@@ -262,9 +262,7 @@ def main():
     torch.cuda.synchronize()
 
     decode = T <= mira.MIRA_DECODE_MAX_TOKENS
-    # one-shot decode calls of at most five tokens route inside the gate/up kernel
-    fused = decode and T <= 5 and 3 * T * (cfg.C + 16) <= 65536
-    dominant = ("decode_route_gateup" if fused else "decode_gateup") if decode else "prefill_gateup"
+    dominant = "decode_gateup" if decode else "prefill_gateup"
     if not args.no_profile:
         # only the dominant kernel carries event records (events cost time)
         mira.mira_profile_select(dominant)
@@ -293,9 +291,6 @@ def main():
             cnt, tot = prof.get(name, (0, 0.0))
             if cnt:
                 dur = tot / cnt * 1e-3
-                # the fused kernel also reads the router weights and x
-                extra = (cfg.E * cfg.C + T * cfg.C) * (4 if cfg.act == "f32" else 2) if fused else 0
-                avg["gu_bytes"] += extra
                 achieved = avg["gu_bytes"] / dur / 1e9
                 roof = {"bound": "hbm", "kernel": name, "achieved": round(achieved, 1),
                         "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),

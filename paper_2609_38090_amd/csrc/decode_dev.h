@@ -1,6 +1,5 @@
-// Device body of the small-batch (decode) gate/up kernels, shared by the
-// kernel that reads the digits of x from the workspace and the kernel that
-// routes the tokens itself.
+// Device body of the small-batch (decode) gate/up kernel: one block of 64
+// expert rows for the tokens of one expert group.
 //
 // The paper fuses INT8 dequantization into the expert FFN (sections IV-A and
 // IV-F).  Because the scale sigma_r is shared by gate row r, up row r and down

@@ -403,14 +403,6 @@ int mira_moe_forward(const mira_shape* s, const mira_moe_args* a, hipStream_t st
   int rc = check_args(s, a, &L);
   if (rc) return rc;
   if (a->n_tokens == 0) return ok();
-  if (use_decode(*s, L.T) && mira::decode_fused_ok(L)) {
-    // routing inside the gate/up kernel, then the down kernel
-    mira::WsPtr w = mira::ws_ptrs(L, a->workspace);
-    HIP_TRY(mira::launch_decode_fused(*s, L, w, a->x, a->w_router, a->router_bias, a->logits,
-                                      pool_of(a), a->expert_counts, a->topk_idx, a->topk_weight,
-                                      a->expert_offsets, a->pair_order, a->out, stream));
-    return ok();
-  }
   rc = run_route(s, a, L, stream);
   if (rc) return rc;
   rc = run_experts(s, a, L, stream);

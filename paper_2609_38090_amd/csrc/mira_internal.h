@@ -224,14 +224,6 @@ hipError_t launch_decode(const mira_shape& s, const Layout& L, const WsPtr& w, c
                          const ExpertPool& ep, float* out, hipStream_t st);
 hipError_t launch_decode_down(const Layout& L, const WsPtr& w, const ExpertPool& ep, float* out,
                               hipStream_t st);
-// One-shot decode call of at most five tokens: routing fused into the gate/up
-// kernel, then the down kernel.  decode_fused_ok says whether a layout qualifies.
-bool decode_fused_ok(const Layout& L);
-hipError_t launch_decode_fused(const mira_shape& s, const Layout& L, const WsPtr& w,
-                               const void* x, const void* wr, const float* bias, float* logits_out,
-                               const ExpertPool& ep, int32_t* counts_out, int32_t* idx_out,
-                               float* wts_out, int32_t* offsets_out, int32_t* order_out,
-                               float* out, hipStream_t st);
 hipError_t launch_prefill(const mira_shape& s, const Layout& L, const WsPtr& w, const void* x,
                           const ExpertPool& ep, float* out, hipStream_t st);
 hipError_t launch_pack(int C, int R, int n, int w_dtype, const void* wg, const void* wu,

@@ -1,7 +1,6 @@
-// Device-side routing helpers shared by the routing kernels and the fused
-// decode kernel: router logits for up to 16 tokens, top-k by rank counting
-// with the combine weights, and the one-wave stable grouping of a decode
-// call's (token, slot) pairs (paper section II-A: the router scores every
+// Device-side routing helpers of the routing kernels: router logits for up
+// to 16 tokens, top-k by rank counting with the combine weights, and the
+// one-wave stable grouping of a decode call's (token, slot) pairs (paper section II-A: the router scores every
 // expert, the top-k experts process the token, their outputs are combined).
 #pragma once
 
@@ -141,88 +140,49 @@ __device__ void logits_ksplit_bf16(const uint16_t* __restrict__ x, const uint16_
   }
 }
 
-// The logits of logits_ksplit_bf16 from a workgroup of NW < 16 waves: wave w
-// computes the partial sums of k-range slices w*16/NW .. (w+1)*16/NW - 1, each
-// with the chunk order and MFMA chain of one wave of the 16-wave split, and
-// the 16 partials are reduced in slice order, so both shapes give
-// bit-identical logits (and the same max |x| per token).  bias_s must be in
-// LDS before the call; only rows t < T of lg are written, xmax needs 16 entries.
-template <int NW>
-__device__ void logits_slices_bf16(const uint16_t* __restrict__ x, const uint16_t* __restrict__ wr,
-                                   const float* bias_s, int T, int E, int C,
-                                   float (*part)[16][17], float (*lg)[MIRA_MAX_EXPERTS],
-                                   float* xmax) {
-  static_assert(kBigWaves % NW == 0, "slices per wave");
-  constexpr int VPW = kBigWaves / NW;
-  constexpr int B = 8;  // chunks per batch, as in the 16-wave split
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int r16 = lane & 15, kg = lane >> 4;
-  const int n_et = (E + 15) / 16, nch = C / 32;
-  const bool tok_ok = r16 < T;
-  const uint16_t* xrow = x + (size_t)(tok_ok ? r16 : 0) * C + kg * 8;
-  for (int et = 0; et < n_et; ++et) {
-    const int e = et * 16 + r16;
-    const bool e_ok = e < E;
-    const uint16_t* wrow = wr + (size_t)(e_ok ? e : 0) * C + kg * 8;
-    for (int j = 0; j < VPW; ++j) {
-      const int vw = wave * VPW + j;
-      v4f acc = {0.f, 0.f, 0.f, 0.f};
-      float xm = 0.f;
-      for (int ch0 = vw; ch0 < nch; ch0 += B * kBigWaves) {
-        v4i a[B], b[B];
-#pragma unroll
-        for (int u = 0; u < B; ++u) {
-          const int ch = ch0 + u * kBigWaves;
-          a[u] = (ch < nch && e_ok) ? ld16(wrow + ch * 32) : zero16();
-          b[u] = (ch < nch && tok_ok) ? ld16(xrow + ch * 32) : zero16();
-        }
-#pragma unroll
-        for (int u = 0; u < B; ++u) {
-          acc = mfma_bf16(a[u], b[u], acc);
-          if (et == 0) xm = fmaxf(xm, absmax_bf16x8(b[u]));
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) part[vw][r16][kg * 4 + i] = acc[i];  // [token][expert]
-      if (et == 0) {
-        xm = fmaxf(xm, __shfl_xor(xm, 16, 64));
-        xm = fmaxf(xm, __shfl_xor(xm, 32, 64));
-        if (kg == 0) part[vw][r16][16] = xm;
-      }
-    }
-    __syncthreads();
-    if (et == 0 && xmax && tid < 16) {
-      float m = 0.f;
-      for (int w = 0; w < kBigWaves; ++w) m = fmaxf(m, part[w][tid][16]);
-      xmax[tid] = m;
-    }
-    for (int i = tid; i < 256; i += NW * 64) {
-      const int tt = i >> 4, ee = i & 15, e2 = et * 16 + ee;
-      float sum = 0.f;
-      for (int w = 0; w < kBigWaves; ++w) sum += part[w][tt][ee];
-      if (e2 < E && tt < T) lg[tt][e2] = sum + (bias_s ? bias_s[e2] : 0.f);
-    }
-    __syncthreads();
-  }
-}
-
 // Top-k of one token by rank counting (one wave): expert e is selected at
 // position rank(e) = number of experts with a larger (value, then lower
-// index) key, if that is < k.  Every lane reads the logits by LDS broadcast,
-// so no cross-lane shuffles are needed.  sel_e/sel_v: this wave's LDS scratch.
+// index) key, if that is < k.  Each lane holds the logits of its experts
+// (lane, lane+64, ...) in registers and takes every other expert's key with
+// v_readlane, so the count needs no memory round trips.  The combine weights
+// are a softmax in fp32, summed in selection order.  sel_e/sel_v: this wave's
+// LDS scratch.
 __device__ __forceinline__ void topk_rank(const float* lgrow, int E, int k, int softmax_all,
                                           int32_t* idx_a, float* w_a, int* sel_e, float* sel_v) {
+  constexpr int kPer = MIRA_MAX_EXPERTS / 64;  // experts per lane
   const int lane = threadIdx.x & 63;
-  for (int e = lane; e < E; e += 64) {
-    const uint32_t ke = f32_order_key(lgrow[e]);
-    int rank = 0;
-    for (int e2 = 0; e2 < E; ++e2) {
-      const uint32_t k2 = f32_order_key(lgrow[e2]);
-      rank += (k2 > ke) || (k2 == ke && e2 < e);
+  const int nblk = (E + 63) / 64;
+  // each lane keeps the logits of experts lane, lane+64, ... in registers;
+  // the comparison keys of the other experts come from v_readlane
+  float val[kPer];
+  uint32_t key[kPer];
+  int rank[kPer];
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int e = lane + 64 * i;
+    val[i] = e < E ? lgrow[e] : 0.f;
+    key[i] = f32_order_key(val[i]);
+    rank[i] = 0;
+  }
+#pragma unroll
+  for (int i2 = 0; i2 < kPer; ++i2) {
+    if (i2 >= nblk) break;
+    const int n2 = min(64, E - 64 * i2);
+#pragma unroll 1
+    for (int l2 = 0; l2 < n2; ++l2) {
+      const uint32_t k2 = (uint32_t)__builtin_amdgcn_readlane((int)key[i2], l2);
+      const int e2 = 64 * i2 + l2;
+#pragma unroll
+      for (int i = 0; i < kPer; ++i)
+        if (i < nblk) rank[i] += (k2 > key[i]) || (k2 == key[i] && e2 < lane + 64 * i);
     }
-    if (rank < k) {
-      sel_e[rank] = e;
-      sel_v[rank] = lgrow[e];
+  }
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int e = lane + 64 * i;
+    if (e < E && rank[i] < k) {
+      sel_e[rank[i]] = e;
+      sel_v[rank[i]] = val[i];
     }
   }
   __builtin_amdgcn_wave_barrier();
@@ -230,9 +190,12 @@ __device__ __forceinline__ void topk_rank(const float* lgrow, int E, int k, int 
   float denom = 0.f;
   if (softmax_all) {
     float s = 0.f;
-    for (int e = lane; e < E; e += 64) s += expf(lgrow[e] - vmax);
+#pragma unroll
+    for (int i = 0; i < kPer; ++i)
+      if (lane + 64 * i < E) s += expf(val[i] - vmax);
     denom = wave_sum(s);
   } else {
+#pragma unroll 1
     for (int j = 0; j < k; ++j) denom += expf(sel_v[j] - vmax);
   }
   if (lane < k) {
