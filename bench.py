@@ -3,8 +3,11 @@
 python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 
 A step is one MoE layer call (router, top-k, permutation, expert FFN over
-packed experts, combine) on one batch of the workload; the beam workload's
-step also runs the predictor head.  Inputs are seeded synthetic tensors of
+packed experts, combine) on one batch of the workload.  The beam workload's
+step is one decode step of its 8 beams through all 32 layers of the stack,
+with 4 of 8 experts per layer resident (HOT slots), the others copied from
+pinned host memory into STAGE slots ahead of time (predictor head for layer
+l+2, or the true experts as an upper bound) or on demand.  Inputs are seeded synthetic tensors of
 the workload's shapes, resident in HBM before timing starts.  Weights are
 rotated over several packed copies of the layer so every call streams cold
 expert bytes (more than 1 GB between reuses, above the 256 MB Infinity Cache).
@@ -72,6 +75,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-profile", action="store_true", help="skip the per-kernel HIP-event timing")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample")
+    p.add_argument("--layers", type=int, default=0, help="layers of the beam stack (0 = all)")
+    p.add_argument("--stage-slots", type=int, default=8, help="STAGE slots of the beam stack")
     p.add_argument("--copy-bytes", type=int, default=0,
                    help="instead of the MoE step, time a plain device-to-device copy of this many "
                         "bytes (the reference kernel for scaling the FETCH_SIZE/WRITE_SIZE counters)")
@@ -198,6 +203,130 @@ def cpu_baseline(cfg, copy0, budget_s):
     }
 
 
+def build_stack(cfg, n_layers, n_stage):
+    """The beam workload's stack: per layer its seeded input, router, HOT experts
+    packed into their device slots and the other experts packed into pinned host
+    memory (one blob each), plus the predictor head scoring layer l+2."""
+    import torch
+    import paper_2609_38090_amd as mira
+    from paper_2609_38090_amd.stack import ExpertStack, LayerData
+    from mira_inputs import (activations, expert_weights, predictor_weights, resident_experts,
+                             router_bias, router_weights)
+
+    stride = mira.mira_packed_expert_bytes(cfg.C, cfg.R)
+    pack_shape = mira.MoEShape(cfg.C, cfg.R, 1, 1)
+    layers = []
+    for l in range(n_layers):
+        b = router_bias(cfg, l)
+        pred = tuple(t.cuda() for t in predictor_weights(cfg, l, "cpu")) if l + 2 < n_layers else None
+        layers.append(LayerData(x=activations(cfg, l, "cuda"), w_router=router_weights(cfg, l, "cuda"),
+                                bias=None if b is None else b.cuda(), hot=resident_experts(cfg, l), pred=pred))
+    shape = mira.MoEShape(cfg.C, cfg.R, cfg.E, cfg.k, cfg.S, mira.MIRA_BF16, 0)
+    ps = mira.PredShape(cfg.C, cfg.pred_hidden, cfg.E, cfg.pred_group, mira.MIRA_BF16)
+    stack = ExpertStack(shape, cfg.T, layers, stride, n_stage=n_stage, pred_shape=ps)
+    n_cold = sum(cfg.E - len(ld.hot) for ld in layers)
+    host = torch.empty(n_cold * stride, dtype=torch.uint8, pin_memory=True)
+    tmp = torch.empty(stride, dtype=torch.uint8, device="cuda")
+    c = 0
+    for l, ld in enumerate(layers):
+        for e in range(cfg.E):
+            wg, wu, wd = expert_weights(cfg, l, e, "cuda")
+            hot = e in stack.hot_slot[l]
+            dst = stack.pool[stack.hot_slot[l][e] * stride:] if hot else tmp
+            mira.mira_pack_experts(pack_shape, 1, mira.MIRA_F32, wg, wu, wd, 1e-8, dst, stride, 1)
+            if not hot:
+                blob = host[c * stride:(c + 1) * stride]
+                blob.copy_(tmp)
+                ld.host[e] = blob
+                c += 1
+            del wg, wu, wd
+    torch.cuda.synchronize()
+    return stack, stride
+
+
+def run_stack(args, cfg):
+    """Beam workload: one decode step of the 8 beams through every layer of the
+    stack, experts served from HOT slots, STAGE slots filled ahead of time, or
+    demand copies; reported per mode of the staging policy."""
+    import torch
+    import paper_2609_38090_amd as mira
+    from paper_2609_38090_amd.stack import StepStats
+
+    mira.load()
+    L = args.layers or cfg.layers
+    t_build = time.perf_counter()
+    stack, stride = build_stack(cfg, L, args.stage_slots)
+    build_s = time.perf_counter() - t_build
+    # the true routing of every layer (the oracle-prefetch mode stages it)
+    true_idx, active = [], []
+    for l in range(L):
+        mira.mira_moe_route(stack.shape, stack.args(l))
+        torch.cuda.synchronize()
+        true_idx.append(stack.idx.cpu().numpy().copy())
+        active.append(len(set(true_idx[-1].reshape(-1).tolist())))
+    steps = max(1, min(args.steps, 8))
+    warm = max(1, min(args.warmup, 2))
+    modes = {}
+    prof = {}
+    for mode in ("predict", "oracle", "demand"):
+        stack.reset_stage()
+        for _ in range(warm):
+            stack.step(mode, true_idx=true_idx)
+        if mode == "predict" and not args.no_profile:
+            mira.mira_profile_select("decode_gateup")
+            mira.mira_profile_enable(True)
+            mira.mira_profile_read()
+        tot = StepStats()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            tot.add(stack.step(mode, true_idx=true_idx))
+        torch.cuda.synchronize()
+        el = (time.perf_counter() - t0) / steps
+        if mode == "predict" and not args.no_profile:
+            prof = mira.mira_profile_read()
+            mira.mira_profile_enable(False)
+        per = {k: getattr(tot, k) / steps for k in tot.__dataclass_fields__}
+        modes[mode] = dict(
+            ms_per_step=round(el * 1e3, 3), tokens_per_s=round(cfg.T / el, 2),
+            layer_tokens_per_s=round(cfg.T * L / el, 2),
+            hot_hits=per["hot_hits"], stage_hits=per["stage_hits"], misses=per["misses"],
+            prefetches=per["prefetches"], prefetch_skipped=per["prefetch_skipped"],
+            h2d_gb_per_step=round(per["h2d_bytes"] / 1e9, 3),
+            h2d_gbs_busy=round(per["h2d_bytes"] / max(per["copy_ms"], 1e-9) / 1e6, 1),
+            h2d_gbs_wall=round(per["h2d_bytes"] / el / 1e9, 1),
+            stall_ms_per_step=round(per["stall_ms"], 3),
+        )
+    ms = modes["predict"]["ms_per_step"]
+    gu_bytes = sum(a * (2 * cfg.R * cfg.C + 2 * cfg.R) for a in active) / L
+    roof = None
+    cnt, tot_ms = prof.get("decode_gateup", (0, 0.0))
+    if cnt:
+        dur = tot_ms / cnt * 1e-3
+        achieved = gu_bytes / dur / 1e9
+        roof = {"bound": "hbm", "kernel": "decode_gateup", "achieved": round(achieved, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": None, "avg_us": round(dur * 1e6, 2),
+                "algorithmic_bytes_per_launch": int(gu_bytes)}
+    line = {
+        "metric": METRIC, "value": modes["predict"]["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1,
+        "steps": steps, "warmup": warm, "ms_per_step": ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "i8", "data": "synthetic",
+        "config": {"workload": cfg.name, "tokens": cfg.T, "layers": L, "hidden": cfg.C,
+                   "experts": cfg.E, "top_k": cfg.k, "ffn": cfg.R, "resident_per_layer": cfg.resident,
+                   "stage_slots": args.stage_slots, "predictor": f"{cfg.C}->{cfg.pred_hidden}->{cfg.E}",
+                   "activations": cfg.act, "experts_selected_per_layer": round(sum(active) / L, 2)},
+        "staging": modes,
+        "setup_s": round(build_s, 1),
+        "kernels_us": {k: round(v[1] / v[0] * 1e3, 2) for k, v in prof.items() if v[0]},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        ld = stack.layers[0]
+        line["cpu_baseline"] = cpu_baseline(cfg, dict(x=ld.x, wr=ld.w_router, bias=ld.bias), args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -216,6 +345,8 @@ def main():
 
     mira.load()
     cfg = CONFIGS[args.workload]
+    if cfg.layers > 1:
+        return run_stack(args, cfg)
     # bytes of packed experts one call can touch: at most min(G, T*k + S) experts
     touched = min(cfg.G, cfg.T * cfg.k + cfg.S) * mira.mira_packed_expert_bytes(cfg.C, cfg.R)
     n_copies = max(2, min(8, math.ceil(COLD_BYTES / max(1, touched)) + 1))
