@@ -42,25 +42,28 @@ COLD_BYTES = 1 << 30
 # shared headers); otherwise the bench reports traffic as null.
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 TRAFFIC = {
-    ("decode_gateup", "mixtral_decode"): dict(source="decode.hip", sha="b3f55c96603ec124",
-                                               fetch_kib=114818.7, write_kib=98.0),
-    ("prefill_gateup", "mixtral_prefill"): dict(source="prefill.hip", sha="818709c58f855a88",
-                                                 fetch_kib=601160.9, write_kib=38316.5),
+    ("decode_gateup", "mixtral_decode"): dict(sources=("decode.hip", "decode_dev.h"), sha="ae857e8dd1f46f20",
+                                               fetch_kib=114811.3, write_kib=98.0),
+    ("prefill_gateup", "mixtral_prefill"): dict(sources=("prefill.hip",), sha="3e60b10b4e04359c",
+                                                 fetch_kib=601387.7, write_kib=38177.1),
 }
+
+
+def source_hash(sources):
+    """Hash of the kernel sources and the two shared headers."""
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2609_38090_amd", "csrc")
+    h = hashlib.sha256()
+    for f in tuple(sources) + ("device_util.h", "mira_internal.h"):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def traffic_bytes(kernel, workload):
     """Counter-measured HBM bytes per launch, or None if not measured on these sources."""
-    import hashlib
     ent = TRAFFIC.get((kernel, workload))
-    if ent is None:
-        return None
-    csrc = os.path.join(ROOT, "paper_2609_38090_amd", "csrc")
-    h = hashlib.sha256()
-    for f in (ent["source"], "device_util.h", "mira_internal.h"):
-        with open(os.path.join(csrc, f), "rb") as fh:
-            h.update(fh.read())
-    if h.hexdigest()[:16] != ent["sha"]:
+    if ent is None or ent["sha"] is None or source_hash(ent["sources"]) != ent["sha"]:
         return None
     return int((ent["fetch_kib"] * FETCH_SCALE + ent["write_kib"] * WRITE_SCALE) * 1024)
 
@@ -77,6 +80,8 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample")
     p.add_argument("--layers", type=int, default=0, help="layers of the beam stack (0 = all)")
     p.add_argument("--stage-slots", type=int, default=8, help="STAGE slots of the beam stack")
+    p.add_argument("--source-hash", action="store_true",
+                   help="print the source hashes the traffic table is keyed on and exit")
     p.add_argument("--copy-bytes", type=int, default=0,
                    help="instead of the MoE step, time a plain device-to-device copy of this many "
                         "bytes (the reference kernel for scaling the FETCH_SIZE/WRITE_SIZE counters)")
@@ -336,6 +341,9 @@ def main():
               "of this build (see the sharding notes in DESIGN.md).", file=sys.stderr)
         return 2
 
+    if args.source_hash:
+        print(json.dumps({f"{k[0]}/{k[1]}": source_hash(v["sources"]) for k, v in TRAFFIC.items()}))
+        return 0
     if args.copy_bytes:
         return copy_reference(args.copy_bytes, args.steps)
 
