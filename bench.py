@@ -80,6 +80,8 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample")
     p.add_argument("--layers", type=int, default=0, help="layers of the beam stack (0 = all)")
     p.add_argument("--stage-slots", type=int, default=8, help="STAGE slots of the beam stack")
+    p.add_argument("--drift-steps", type=int, default=36,
+                   help="beam stack: steps of the drifting-popularity HOT rebalancing run (0 = skip)")
     p.add_argument("--source-hash", action="store_true",
                    help="print the source hashes the traffic table is keyed on and exit")
     p.add_argument("--copy-bytes", type=int, default=0,
@@ -208,10 +210,12 @@ def cpu_baseline(cfg, copy0, budget_s):
     }
 
 
-def build_stack(cfg, n_layers, n_stage):
+def build_stack(cfg, n_layers, n_stage, hot=None, bias=None, host_all=False, rebalancer=None):
     """The beam workload's stack: per layer its seeded input, router, HOT experts
-    packed into their device slots and the other experts packed into pinned host
-    memory (one blob each), plus the predictor head scoring layer l+2."""
+    packed into their device slots and the other experts (all of them if
+    host_all, as a rebalancer may evict and later promote any expert) packed
+    into pinned host memory, one blob each, plus the predictor head scoring
+    layer l+2.  hot(l) and bias(l) override the workload's HOT set and bias."""
     import torch
     import paper_2609_38090_amd as mira
     from paper_2609_38090_amd.stack import ExpertStack, LayerData
@@ -222,24 +226,27 @@ def build_stack(cfg, n_layers, n_stage):
     pack_shape = mira.MoEShape(cfg.C, cfg.R, 1, 1)
     layers = []
     for l in range(n_layers):
-        b = router_bias(cfg, l)
+        b = router_bias(cfg, l) if bias is None else bias(l)
         pred = tuple(t.cuda() for t in predictor_weights(cfg, l, "cpu")) if l + 2 < n_layers else None
         layers.append(LayerData(x=activations(cfg, l, "cuda"), w_router=router_weights(cfg, l, "cuda"),
-                                bias=None if b is None else b.cuda(), hot=resident_experts(cfg, l), pred=pred))
+                                bias=None if b is None else b.cuda(),
+                                hot=resident_experts(cfg, l) if hot is None else hot(l), pred=pred))
     shape = mira.MoEShape(cfg.C, cfg.R, cfg.E, cfg.k, cfg.S, mira.MIRA_BF16, 0)
     ps = mira.PredShape(cfg.C, cfg.pred_hidden, cfg.E, cfg.pred_group, mira.MIRA_BF16)
-    stack = ExpertStack(shape, cfg.T, layers, stride, n_stage=n_stage, pred_shape=ps)
-    n_cold = sum(cfg.E - len(ld.hot) for ld in layers)
-    host = torch.empty(n_cold * stride, dtype=torch.uint8, pin_memory=True)
+    stack = ExpertStack(shape, cfg.T, layers, stride, n_stage=n_stage, pred_shape=ps, rebalancer=rebalancer)
+    n_host = sum(cfg.E if host_all else cfg.E - len(ld.hot) for ld in layers)
+    host = torch.empty(n_host * stride, dtype=torch.uint8, pin_memory=True)
     tmp = torch.empty(stride, dtype=torch.uint8, device="cuda")
     c = 0
     for l, ld in enumerate(layers):
         for e in range(cfg.E):
             wg, wu, wd = expert_weights(cfg, l, e, "cuda")
-            hot = e in stack.hot_slot[l]
-            dst = stack.pool[stack.hot_slot[l][e] * stride:] if hot else tmp
-            mira.mira_pack_experts(pack_shape, 1, mira.MIRA_F32, wg, wu, wd, 1e-8, dst, stride, 1)
-            if not hot:
+            is_hot = e in stack.hot_slot[l]
+            mira.mira_pack_experts(pack_shape, 1, mira.MIRA_F32, wg, wu, wd, 1e-8, tmp, stride, 1)
+            if is_hot:
+                slot = stack.hot_slot[l][e]
+                stack.pool[slot * stride:(slot + 1) * stride].copy_(tmp)
+            if host_all or not is_hot:
                 blob = host[c * stride:(c + 1) * stride]
                 blob.copy_(tmp)
                 ld.host[e] = blob
@@ -247,6 +254,50 @@ def build_stack(cfg, n_layers, n_stage):
             del wg, wu, wd
     torch.cuda.synchronize()
     return stack, stride
+
+
+def run_drift(cfg, n_layers, steps, period):
+    """HOT rebalancing on a workload whose expert popularity drifts: every
+    `period` steps the Zipf ranks of every layer's router bias change.  The
+    same inputs run with a static HOT set (the popular experts of the first
+    period) and with the telemetry-driven rebalancer; experts outside HOT are
+    copied on demand (no prefetch), so the difference is the HOT hit rate."""
+    import torch
+    from paper_2609_38090_amd.policy import RebalanceConfig, Rebalancer
+    from paper_2609_38090_amd.stack import StepStats
+    from mira_inputs import activations, drift_bias, drift_hot
+
+    res = {}
+    for name in ("static", "rebalanced"):
+        rb = Rebalancer(RebalanceConfig(interval=64, max_swaps=1, probation=2)) if name == "rebalanced" else None
+        stack, _ = build_stack(cfg, n_layers, max(cfg.E - cfg.resident, 4) + 2,
+                               hot=lambda l: drift_hot(cfg, l, 0, cfg.resident),
+                               bias=lambda l: drift_bias(cfg, l, 0), host_all=True, rebalancer=rb)
+        per_epoch = []
+        t0 = time.perf_counter()
+        for s in range(steps):
+            ep = s // period
+            for l, ld in enumerate(stack.layers):
+                ld.x.copy_(activations(cfg, l, "cuda", base=1 + s))
+                ld.bias.copy_(drift_bias(cfg, l, ep).cuda())
+            st = stack.step("demand")
+            if s % period == 0:
+                per_epoch.append(StepStats())
+            per_epoch[-1].add(st)
+        el = time.perf_counter() - t0
+        eps = []
+        for ep, st in enumerate(per_epoch):
+            tok = st.hot_tokens + st.stage_tokens + st.cpu_tokens
+            eps.append(dict(epoch=ep, hot_token_share=round(st.hot_tokens / max(tok, 1), 3),
+                            misses_per_step=round(st.misses / period, 2), swaps=st.swaps,
+                            h2d_gb_per_step=round(st.h2d_bytes / period / 1e9, 3),
+                            ms_per_step=round(st.wall_ms / period, 2)))
+        res[name] = dict(epochs=eps, ms_per_step=round(el * 1e3 / steps, 2))
+        del stack
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+    return dict(layers=n_layers, steps=steps, period=period, rebalance="interval 64 tokens, 1 swap, probation 2",
+                **res)
 
 
 def run_stack(args, cfg):
@@ -295,7 +346,8 @@ def run_stack(args, cfg):
             ms_per_step=round(el * 1e3, 3), tokens_per_s=round(cfg.T / el, 2),
             layer_tokens_per_s=round(cfg.T * L / el, 2),
             hot_hits=per["hot_hits"], stage_hits=per["stage_hits"], misses=per["misses"],
-            prefetches=per["prefetches"], prefetch_skipped=per["prefetch_skipped"],
+            prefetches=per["prefetches"], prefetch_cached=per["prefetch_cached"],
+            prefetch_declined=per["prefetch_declined"],
             h2d_gb_per_step=round(per["h2d_bytes"] / 1e9, 3),
             h2d_gbs_busy=round(per["h2d_bytes"] / max(per["copy_ms"], 1e-9) / 1e6, 1),
             h2d_gbs_wall=round(per["h2d_bytes"] / el / 1e9, 1),
@@ -325,6 +377,8 @@ def run_stack(args, cfg):
         "kernels_us": {k: round(v[1] / v[0] * 1e3, 2) for k, v in prof.items() if v[0]},
         "roofline": roof,
     }
+    if args.drift_steps > 0:
+        line["drift"] = run_drift(cfg, min(L, 8), args.drift_steps, max(1, args.drift_steps // 3))
     if not args.no_cpu_baseline:
         ld = stack.layers[0]
         line["cpu_baseline"] = cpu_baseline(cfg, dict(x=ld.x, wr=ld.w_router, bias=ld.bias), args.cpu_seconds)

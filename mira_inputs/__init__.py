@@ -12,6 +12,8 @@ expert of any layer can be regenerated alone, on the host or on the device.
 from .configs import CONFIGS, MoEConfig, get_config  # noqa: F401
 from .gen import (  # noqa: F401
     activations,
+    drift_bias,
+    drift_hot,
     router_weights,
     router_bias,
     expert_weights,

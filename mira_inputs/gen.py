@@ -89,3 +89,19 @@ def predictor_weights(cfg: MoEConfig, layer: int, device="cpu"):
     b1 = torch.zeros(P, dtype=torch.float32, device=device)
     b2 = torch.zeros(cfg.E, dtype=torch.float32, device=device)
     return w1.to(torch.bfloat16), b1, w2.to(torch.bfloat16), b2
+
+
+def drift_bias(cfg: MoEConfig, layer: int, epoch: int):
+    """Router bias of a workload whose expert popularity drifts: the Zipf-ranked
+    bias -s * ln(rank(e) + 1) with a seeded rank permutation per (layer, epoch)."""
+    rng = np.random.Generator(np.random.PCG64(tensor_seed(cfg, layer, epoch, _RANK, base=7)))
+    rank = rng.permutation(cfg.E)
+    b = np.array([-cfg.zipf_s * math.log(r + 1.0) for r in rank], dtype=np.float32)
+    return torch.from_numpy(b)
+
+
+def drift_hot(cfg: MoEConfig, layer: int, epoch: int, n: int):
+    """The n most popular experts of a drifting layer in one epoch."""
+    rng = np.random.Generator(np.random.PCG64(tensor_seed(cfg, layer, epoch, _RANK, base=7)))
+    rank = rng.permutation(cfg.E)
+    return sorted(int(e) for e in np.argsort(rank, kind="stable")[:n])

@@ -17,18 +17,19 @@ SMALL_STACK = MoEConfig("small_stack", 104, T=8, C=128, E=8, k=2, R=192, zipf_s=
                         pred_hidden=32, pred_group=8)
 
 
-def build(mira, cfg, n_stage):
+def build(mira, cfg, n_stage, hot=None, bias=None, host_all=False, rebalancer=None):
     from paper_2609_38090_amd.stack import ExpertStack, LayerData
     stride = mira.mira_packed_expert_bytes(cfg.C, cfg.R)
     layers, blobs = [], {}
     for l in range(cfg.layers):
-        b = router_bias(cfg, l)
+        b = router_bias(cfg, l) if bias is None else bias(l)
         pred = tuple(t.cuda() for t in predictor_weights(cfg, l, "cpu")) if l + 2 < cfg.layers else None
         layers.append(LayerData(x=activations(cfg, l, "cuda"), w_router=router_weights(cfg, l, "cuda"),
-                                bias=None if b is None else b.cuda(), hot=resident_experts(cfg, l), pred=pred))
+                                bias=None if b is None else b.cuda(),
+                                hot=resident_experts(cfg, l) if hot is None else hot(l), pred=pred))
     shape = mira.MoEShape(cfg.C, cfg.R, cfg.E, cfg.k, cfg.S, mira.MIRA_BF16, 0)
     ps = mira.PredShape(cfg.C, cfg.pred_hidden, cfg.E, cfg.pred_group, mira.MIRA_BF16)
-    st = ExpertStack(shape, cfg.T, layers, stride, n_stage=n_stage, pred_shape=ps)
+    st = ExpertStack(shape, cfg.T, layers, stride, n_stage=n_stage, pred_shape=ps, rebalancer=rebalancer)
     pack_shape = mira.MoEShape(cfg.C, cfg.R, 1, 1)
     for l, ld in enumerate(layers):
         for e in range(cfg.E):
@@ -39,7 +40,7 @@ def build(mira, cfg, n_stage):
                                    w[2].ctypes.data, EPS, pinned, stride, 0)
             if e in st.hot_slot[l]:
                 st.pool[st.hot_slot[l][e] * stride:(st.hot_slot[l][e] + 1) * stride].copy_(pinned)
-            else:
+            if host_all or e not in st.hot_slot[l]:
                 ld.host[e] = pinned
     torch.cuda.synchronize()
     return st, blobs
@@ -92,3 +93,35 @@ def test_stack_modes_agree_and_match_oracle(mira, n_stage):
         ref = oracle.moe_forward(x, wr, b, [blobs[l, e] for e in range(cfg.E)], cfg.k, cfg.C, cfg.R)
         assert np.array_equal(ref["idx"], true_idx[l])
         assert_ffn_close(base[l], ref["out"], f"stack layer {l}")
+
+
+def test_rebalancer_tracks_drift_without_changing_outputs(mira):
+    """Expert popularity moves at step 6; the rebalanced stack must swap the
+    new popular experts into HOT (telemetry, probation, bounded swaps) while
+    every layer output stays bit-identical to the stack whose HOT set is fixed."""
+    from paper_2609_38090_amd.policy import RebalanceConfig, Rebalancer
+    from mira_inputs import drift_bias, drift_hot
+    cfg = SMALL_STACK
+    hot0 = lambda l: drift_hot(cfg, l, 0, cfg.resident)  # noqa: E731
+    b0 = lambda l: drift_bias(cfg, l, 0)  # noqa: E731
+    fixed, _ = build(mira, cfg, 4, hot=hot0, bias=b0, host_all=True)
+    moving, _ = build(mira, cfg, 4, hot=hot0, bias=b0, host_all=True,
+                      rebalancer=Rebalancer(RebalanceConfig(interval=32, max_swaps=1, probation=2)))
+    swaps = 0
+    for s in range(24):
+        ep = s // 6
+        for st in (fixed, moving):
+            for l, ld in enumerate(st.layers):
+                ld.x.copy_(activations(cfg, l, "cuda", base=1 + s))
+                ld.bias.copy_(drift_bias(cfg, l, ep).cuda())
+        a, _ = run(fixed, "demand")
+        b, stats = run(moving, "demand" if s % 2 else "predict")
+        swaps += stats.swaps
+        for l in range(cfg.layers):
+            assert np.array_equal(a[l], b[l]), (s, l)
+    assert swaps > 0
+    # the rebalanced HOT sets hold more of the last period's popular experts
+    last = [set(drift_hot(cfg, l, 3, cfg.resident)) for l in range(cfg.layers)]
+    got_fixed = sum(len(fixed.hot_set(l) & last[l]) for l in range(cfg.layers))
+    got_moving = sum(len(moving.hot_set(l) & last[l]) for l in range(cfg.layers))
+    assert got_moving > got_fixed, (got_moving, got_fixed)
