@@ -300,6 +300,83 @@ def run_drift(cfg, n_layers, steps, period):
                 **res)
 
 
+MIX_HIST_HIDDEN = 64  # HistHead width of the beam workload's MixtureHeads (ActHead: the MLP's width)
+
+
+def mixture_heads(cfg, n_layers):
+    """MixtureHead of every layer with a layer l+2 (seeded synthetic weights)."""
+    import torch
+    import paper_2609_38090_amd as mira
+    from mira_inputs import mixture_weights
+
+    shape = mira.MixtureShape(cfg.C, cfg.E, cfg.k, cfg.k, cfg.pred_hidden, MIX_HIST_HIDDEN, cfg.E,
+                              cfg.pred_group, mira.MIRA_BF16)
+    heads = []
+    for l in range(n_layers):
+        if l + 2 >= n_layers:
+            heads.append(None)
+            continue
+        W = mixture_weights(cfg, l, cfg.pred_hidden, MIX_HIST_HIDDEN)
+        heads.append(mira.MixtureWeights(**{k: v.cuda() for k, v in W.items() if torch.is_tensor(v)},
+                                         bg=W["bg"]))
+    return shape, heads
+
+
+def head_bytes(cfg, kind, T):
+    """Bytes one predictor call must move: weights, inputs and outputs."""
+    C, E, P, n = cfg.C, cfg.E, cfg.pred_hidden, T // cfg.pred_group
+    if kind == "predict":
+        return 2 * P * C + 4 * P + 2 * E * P + 4 * E + 2 * T * C + 4 * n * E
+    Ph = MIX_HIST_HIDDEN
+    w = 2 * (P * C + P * E + E * P + 2 * Ph * E + E * Ph + C + 3 * E) + 4 * (P + Ph + 2 * E)
+    return w + 2 * T * C + 4 * T * E + 4 * T * cfg.k + 4 * n * (E + 1)
+
+
+def run_heads(cfg, n_layers, stack, heads_mix, mix_shape, reps=50):
+    """Both predictor heads alone: one call per decode step of one layer
+    (the beam's 8 tokens, one group), and all layers' calls batched into one.
+    Per-call time from the library's event pairs around each call."""
+    import torch
+    import paper_2609_38090_amd as mira
+
+    ld = stack.layers[0]
+    T = cfg.T
+    logits = torch.randn((T * n_layers, cfg.E), device="cuda")
+    idx = torch.randint(0, cfg.E, (T * n_layers, cfg.k), dtype=torch.int32, device="cuda")
+    xb = ld.x.repeat(n_layers, 1)
+    ps = mira.PredShape(cfg.C, cfg.pred_hidden, cfg.E, cfg.pred_group, mira.MIRA_BF16)
+    w1, b1, w2, b2 = ld.pred
+    out = {}
+    for tokens in (T, T * n_layers):
+        n = tokens // cfg.pred_group
+        scores = torch.empty((n, cfg.E), device="cuda")
+        pws = torch.empty(max(mira.mira_predict_workspace_bytes(ps, tokens),
+                              mira.mira_mixture_workspace_bytes(mix_shape, tokens)), dtype=torch.uint8,
+                          device="cuda")
+        calls = {
+            "predict": lambda: mira.mira_predict(ps, xb, tokens, w1, b1, w2, b2, scores, pws, pws.numel()),
+            "mixture": lambda: mira.mira_predict_mixture(mix_shape, heads_mix[0], xb, logits, idx, tokens, scores,
+                                                         None, pws, pws.numel()),
+        }
+        for name, fn in calls.items():
+            for _ in range(3):
+                fn()
+            mira.mira_profile_select(name)
+            mira.mira_profile_enable(True)
+            mira.mira_profile_read()
+            for _ in range(reps):
+                fn()
+            cnt, ms = mira.mira_profile_read().get(name, (0, 0.0))
+            mira.mira_profile_enable(False)
+            us = ms / max(cnt, 1) * 1e3
+            nbytes = head_bytes(cfg, name, tokens)
+            out[f"{name}_T{tokens}"] = dict(us_per_call=round(us, 2), predictions=n, bytes=nbytes,
+                                            gbs=round(nbytes / max(us, 1e-9) / 1e3, 1))
+    mira.mira_profile_select(None)
+    torch.cuda.synchronize()
+    return out
+
+
 def run_stack(args, cfg):
     """Beam workload: one decode step of the 8 beams through every layer of the
     stack, experts served from HOT slots, STAGE slots filled ahead of time, or
@@ -353,6 +430,28 @@ def run_stack(args, cfg):
             h2d_gbs_wall=round(per["h2d_bytes"] / el / 1e9, 1),
             stall_ms_per_step=round(per["stall_ms"], 3),
         )
+    # the same policy with the MixtureHead scoring layer l+2
+    mix_shape, heads_mix = mixture_heads(cfg, L)
+    mlp_shape, heads_mlp = stack.pred_shape, [ld.pred for ld in stack.layers]
+    stack.set_predictor(mix_shape, heads_mix)
+    stack.reset_stage()
+    for _ in range(warm):
+        stack.step("predict")
+    tot = StepStats()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        tot.add(stack.step("predict"))
+    torch.cuda.synchronize()
+    el = (time.perf_counter() - t0) / steps
+    per = {k: getattr(tot, k) / steps for k in tot.__dataclass_fields__}
+    modes["predict_mixture"] = dict(
+        ms_per_step=round(el * 1e3, 3), tokens_per_s=round(cfg.T / el, 2),
+        hot_hits=per["hot_hits"], stage_hits=per["stage_hits"], misses=per["misses"],
+        prefetches=per["prefetches"], prefetch_cached=per["prefetch_cached"],
+        prefetch_declined=per["prefetch_declined"], h2d_gb_per_step=round(per["h2d_bytes"] / 1e9, 3),
+        stall_ms_per_step=round(per["stall_ms"], 3))
+    stack.set_predictor(mlp_shape, heads_mlp)
+    heads = run_heads(cfg, L - 2, stack, heads_mix, mix_shape)
     ms = modes["predict"]["ms_per_step"]
     gu_bytes = sum(a * (2 * cfg.R * cfg.C + 2 * cfg.R) for a in active) / L
     roof = None
@@ -373,6 +472,9 @@ def run_stack(args, cfg):
                    "stage_slots": args.stage_slots, "predictor": f"{cfg.C}->{cfg.pred_hidden}->{cfg.E}",
                    "activations": cfg.act, "experts_selected_per_layer": round(sum(active) / L, 2)},
         "staging": modes,
+        "predictor_heads": dict(mixture=f"ActHead {cfg.C}+{cfg.E}->{cfg.pred_hidden}->{cfg.E}, "
+                                        f"HistHead {2 * cfg.E}->{MIX_HIST_HIDDEN}->{cfg.E}, gate {cfg.C + 3 * cfg.E}->1",
+                                **heads),
         "setup_s": round(build_s, 1),
         "kernels_us": {k: round(v[1] / v[0] * 1e3, 2) for k, v in prof.items() if v[0]},
         "roofline": roof,

@@ -10,8 +10,9 @@
  * (sections IV-A and IV-F), and the weighted combine.  Experts are found
  * through a slot table into a caller-owned pool of device slots, the HOT and
  * STAGE regions of the expert cache (section IV-C); slots are filled from
- * pinned host memory by asynchronous copies (sections IV-E, IV-F).  A small
- * predictor head scores the experts of layer l+2 (section IV-E).
+ * pinned host memory by asynchronous copies (sections IV-E, IV-F).  Predictor
+ * heads score the experts of layer l+2 (section IV-E): a two-layer MLP and the
+ * paper's MixtureHead.
  *
  * Conventions for every entry point:
  *  - Return 0 (MIRA_OK) on success or a negative mira_status.  A failing call
@@ -194,12 +195,74 @@ size_t mira_predict_workspace_bytes(const mira_pred_shape* p, int32_t n_tokens);
  *   f_i = mean of rows [i*group, (i+1)*group) of x,
  *   z   = ReLU(W1 f_i + b1),  scores[i] = sigmoid(W2 z + b2),
  * fp32 accumulation.  x [T][C] (act_dtype), T a multiple of group;
- * w1 [P][C] bf16; b1 [P] fp32 or NULL; w2 [n_out][P] bf16; b2 [n_out] fp32 or
+ * w1 [P][C] bf16, 16-byte aligned; b1 [P] fp32 or NULL; w2 [n_out][P] bf16; b2 [n_out] fp32 or
  * NULL; scores [T/group][n_out] fp32.  All device pointers. */
 int mira_predict(const mira_pred_shape* p, const void* x, int32_t n_tokens,
                  const void* w1, const float* b1, const void* w2, const float* b2,
                  float* scores, void* workspace, uint64_t workspace_bytes,
                  hipStream_t stream);
+
+/* ---- MixtureHead predictor (section IV-E) ------------------------------- */
+/* The paper's predictor head: an ActHead over the semantic context and the
+ * router logits and a HistHead over the expert-selection history, each giving
+ * logits over the experts of layer l+2, mixed by a contextual gate alpha.  The
+ * paper names the parts, not their sizes; the widths below are parameters. */
+typedef struct mira_mixture_shape {
+  int32_t hidden;      /* C: multiple of 64 */
+  int32_t n_src;       /* E: experts of the source layer l, 1..MIRA_MAX_EXPERTS */
+  int32_t top_k;       /* k: columns of topk_idx, 1..MIRA_MAX_TOPK */
+  int32_t hist_top;    /* m: most-loaded experts flagged in the top-m feature, 1..n_src */
+  int32_t act_hidden;  /* Pa: hidden width of the ActHead, >= 1 */
+  int32_t hist_hidden; /* Ph: hidden width of the HistHead, >= 1 */
+  int32_t n_out;       /* N: experts of layer l+2, 1..MIRA_MAX_EXPERTS */
+  int32_t group;       /* token rows per prediction, >= 1 */
+  int32_t act_dtype;   /* mira_dtype of x */
+  int32_t reserved;    /* must be 0 */
+} mira_mixture_shape;
+
+/* Weights of one MixtureHead, device pointers.  Matrices and gate vectors are
+ * bf16, row-major; biases are fp32 and may be NULL (zero).  wah and gh must be
+ * 16-byte aligned. */
+typedef struct mira_mixture_weights {
+  const void* wah;  /* [Pa][C]  ActHead layer 1, pooled hidden part */
+  const void* wal;  /* [Pa][E]  ActHead layer 1, mean router-logit part */
+  const float* ba1; /* [Pa] */
+  const void* wa2;  /* [N][Pa]  ActHead output layer */
+  const float* ba2; /* [N] */
+  const void* whq;  /* [Ph][E]  HistHead layer 1, selection-histogram part */
+  const void* whu;  /* [Ph][E]  HistHead layer 1, top-m indicator part */
+  const float* bh1; /* [Ph] */
+  const void* wh2;  /* [N][Ph]  HistHead output layer */
+  const float* bh2; /* [N] */
+  const void* gh;   /* [C]  gate weights on the pooled hidden */
+  const void* gl;   /* [E]  ... on the mean router logits */
+  const void* gq;   /* [E]  ... on the selection histogram */
+  const void* gu;   /* [E]  ... on the top-m indicator */
+  float bg;         /* gate bias */
+  int32_t reserved; /* must be 0 */
+} mira_mixture_weights;
+
+/* Bytes of workspace mira_predict_mixture needs for n_tokens tokens. */
+size_t mira_mixture_workspace_bytes(const mira_mixture_shape* p, int32_t n_tokens);
+
+/* Distribution over layer l+2's experts for each group i of `group` token rows
+ * of layer l (rows [i*group, (i+1)*group)):
+ *   h = mean hidden row, l = mean router-logit row,
+ *   q[e] = (pairs of the group routed to e) / (group * k),
+ *   u[e] = 1 for the m experts with the most routed pairs (count descending,
+ *          index ascending) whose count is positive, else 0,
+ *   a = wa2 ReLU(wah h + wal l + ba1) + ba2        (ActHead logits)
+ *   b = wh2 ReLU(whq q + whu u + bh1) + bh2        (HistHead logits)
+ *   alpha = sigmoid(gh.h + gl.l + gq.q + gu.u + bg) (contextual gate)
+ *   probs[i] = softmax(alpha a + (1 - alpha) b),
+ * fp32 accumulation.  x [T][C] (act_dtype, 16-byte aligned); logits [T][E]
+ * fp32 and topk_idx [T][k] as written by mira_moe_forward for layer l; entries
+ * of topk_idx outside 0..E-1 are not counted.  probs [T/group][N] fp32;
+ * alpha [T/group] fp32 or NULL.  T must be a multiple of group. */
+int mira_predict_mixture(const mira_mixture_shape* p, const mira_mixture_weights* w,
+                         const void* x, const float* logits, const int32_t* topk_idx,
+                         int32_t n_tokens, float* probs, float* alpha, void* workspace,
+                         uint64_t workspace_bytes, hipStream_t stream);
 
 /* ---- expert staging (sections IV-C, IV-E, IV-F) ------------------------- */
 /* Copy one packed expert from pinned host memory into slot `slot` of a slot

@@ -18,6 +18,8 @@ from .gen import (  # noqa: F401
     router_bias,
     expert_weights,
     predictor_weights,
+    mixture_weights,
+    routing_sample,
     resident_experts,
     tensor_seed,
 )

@@ -9,7 +9,7 @@ import torch
 from .configs import MoEConfig
 
 # tensor ids inside a seed tuple
-_X, _WG, _RANK, _GATE, _UP, _DOWN, _PW1, _PW2 = range(8)
+_X, _WG, _RANK, _GATE, _UP, _DOWN, _PW1, _PW2, _ROUTE, _MIX = range(10)
 
 
 def tensor_seed(cfg: MoEConfig, layer: int, expert: int, tensor: int, base: int = 0) -> int:
@@ -105,3 +105,47 @@ def drift_hot(cfg: MoEConfig, layer: int, epoch: int, n: int):
     rng = np.random.Generator(np.random.PCG64(tensor_seed(cfg, layer, epoch, _RANK, base=7)))
     rank = rng.permutation(cfg.E)
     return sorted(int(e) for e in np.argsort(rank, kind="stable")[:n])
+
+
+_MIX_MATS = (("wah", "Pa", "C"), ("wal", "Pa", "E"), ("wa2", "N", "Pa"), ("whq", "Ph", "E"),
+             ("whu", "Ph", "E"), ("wh2", "N", "Ph"), ("gh", None, "C"), ("gl", None, "E"),
+             ("gq", None, "E"), ("gu", None, "E"))
+_MIX_BIAS = (("ba1", "Pa"), ("ba2", "N"), ("bh1", "Ph"), ("bh2", "N"))
+
+
+def mixture_weights(cfg: MoEConfig, layer: int, act_hidden: int, hist_hidden: int,
+                    n_out: int | None = None, device="cpu"):
+    """Synthetic MixtureHead weights for a source layer with cfg.E experts.
+
+    Matrices and gate vectors are bf16 ~ N(0, 1/fan_in) (fan_in = their
+    column count; the gate's over all of C + 3E features), biases fp32
+    ~ N(0, 0.1^2), the gate bias a float ~ N(0, 0.25^2).  Returns a dict keyed
+    like the C struct's fields."""
+    dims = {"C": cfg.C, "E": cfg.E, "Pa": act_hidden, "Ph": hist_hidden,
+            "N": cfg.E if n_out is None else n_out}
+    out = {}
+    for j, (name, rows, cols) in enumerate(_MIX_MATS):
+        fan = dims[cols] if rows else cfg.C + 3 * cfg.E
+        shape = (dims[rows], dims[cols]) if rows else (dims[cols],)
+        t = _randn(shape, tensor_seed(cfg, layer, j, _MIX), device, 1.0 / math.sqrt(fan))
+        out[name] = t.to(torch.bfloat16)
+    for j, (name, size) in enumerate(_MIX_BIAS):
+        out[name] = _randn((dims[size],), tensor_seed(cfg, layer, 100 + j, _MIX), device, 0.1)
+    out["bg"] = float(_randn((1,), tensor_seed(cfg, layer, 200, _MIX), "cpu", 0.25)[0])
+    return out
+
+
+def routing_sample(cfg: MoEConfig, layer: int, T: int | None = None):
+    """A synthetic routing record of a source layer, on the host: logits [T][E]
+    fp32 ~ N(0, 1) and topk_idx [T][k] int32, k distinct experts per token
+    drawn without replacement with Zipf(cfg.zipf_s) popularity over a seeded
+    ranking (uniform if zipf_s is 0)."""
+    T = cfg.T if T is None else T
+    logits = _randn((T, cfg.E), tensor_seed(cfg, layer, 0, _ROUTE), "cpu")
+    rng = np.random.Generator(np.random.PCG64(tensor_seed(cfg, layer, 1, _ROUTE)))
+    rank = rng.permutation(cfg.E)
+    p = (rank + 1.0) ** -cfg.zipf_s
+    p /= p.sum()
+    idx = np.stack([rng.choice(cfg.E, size=cfg.k, replace=False, p=p) for _ in range(T)]) if T else \
+        np.zeros((0, cfg.k), dtype=np.int64)
+    return logits, torch.from_numpy(idx.astype(np.int32))

@@ -36,6 +36,18 @@ notes of the repository):
   order.
 * Predictor (section IV-E, with the MLP shape of the workload): mean-pool a
   group of token rows, z = ReLU(W1 f + b1), scores = sigmoid(W2 z + b2).
+* MixtureHead (section IV-E; the paper names its parts, not their sizes):
+  per group of token rows the features are the mean hidden row h, the mean
+  router logits l, the selection histogram q (tokens routed to each expert of
+  the source layer over the group's (token, slot) pairs, divided by
+  group * k) and the top-m indicator u (1 for the m experts with the most
+  routed tokens, ranked by count descending then index ascending, and only
+  if the count is positive).  ActHead: a = Wa2 ReLU(Wah h + Wal l + ba1) + ba2;
+  HistHead: b = Wh2 ReLU(Whq q + Whu u + bh1) + bh2; contextual gate: one
+  unit over every feature, alpha = sigmoid(gh.h + gl.l + gq.q + gu.u + bg);
+  the two logit vectors are mixed, y = alpha a + (1 - alpha) b, and the
+  output distribution is softmax(y) (the heads are trained with
+  cross-entropy).
 """
 
 from __future__ import annotations
@@ -60,6 +72,8 @@ __all__ = [
     "expert_ffn",
     "moe_forward",
     "predictor_scores",
+    "mixture_features",
+    "mixture_head",
     "coverage_at_k",
 ]
 
@@ -385,6 +399,83 @@ def predictor_scores(x, group: int, w1, b1, w2, b2):
         z = np.maximum(w1 @ f + b1, 0.0)
         scores[i] = 1.0 / (1.0 + np.exp(-(w2 @ z + b2)))
     return scores
+
+
+def mixture_features(x, logits, topk_idx, group: int, n_src: int, m: int):
+    """Features of the MixtureHead for each group of token rows (section IV-E).
+
+    Returns (h, l, q, u): h [n][C] mean hidden row; l [n][E] mean router
+    logits; q [n][E] selection histogram over the group's (token, slot) pairs,
+    as fractions of group * k; u [n][E] indicator of the m experts with the
+    most routed tokens (count descending, index ascending), only for experts
+    with a positive count.  fp64; counts are exact integers.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    logits = np.asarray(logits, dtype=np.float64)
+    topk_idx = np.asarray(topk_idx, dtype=np.int64)
+    T = x.shape[0]
+    if group <= 0 or T % group:
+        raise ValueError("T must be a positive multiple of group")
+    if logits.shape != (T, n_src) or topk_idx.shape[0] != T:
+        raise ValueError("logits must be [T][n_src] and topk_idx [T][k]")
+    if not 1 <= m <= n_src:
+        raise ValueError("m must lie in 1..n_src")
+    if topk_idx.size and (topk_idx.min() < 0 or topk_idx.max() >= n_src):
+        raise ValueError("topk_idx entries must lie in 0..n_src-1")
+    n, k = T // group, topk_idx.shape[1]
+    h = np.empty((n, x.shape[1]))
+    l = np.empty((n, n_src))
+    q = np.zeros((n, n_src))
+    u = np.zeros((n, n_src))
+    for i in range(n):
+        rows = slice(i * group, (i + 1) * group)
+        h[i] = x[rows].mean(axis=0)
+        l[i] = logits[rows].mean(axis=0)
+        counts = np.zeros(n_src, dtype=np.int64)
+        for e in topk_idx[rows].ravel():
+            counts[e] += 1
+        q[i] = counts / float(group * k)
+        ranked = sorted(range(n_src), key=lambda e: (-counts[e], e))
+        for e in ranked[:m]:
+            if counts[e] > 0:
+                u[i, e] = 1.0
+    return h, l, q, u
+
+
+def mixture_head(x, logits, topk_idx, group: int, m: int, weights: dict):
+    """MixtureHead distribution over the experts of layer l+2 (section IV-E).
+
+    weights (fp64 arrays; any bias may be None for zero):
+      wah [Pa][C], wal [Pa][E], ba1 [Pa], wa2 [N][Pa], ba2 [N]   (ActHead)
+      whq [Ph][E], whu [Ph][E], bh1 [Ph], wh2 [N][Ph], bh2 [N]   (HistHead)
+      gh [C], gl [E], gq [E], gu [E], bg (scalar)                (gate)
+    Per group: a and b are the two heads' logits, alpha the gate,
+    y = alpha a + (1 - alpha) b, probs = softmax(y).  Returns a dict with
+    probs [n][N], alpha [n], y [n][N], a [n][N] and b [n][N].  fp64.
+    """
+    W = {k: (None if v is None else np.asarray(v, dtype=np.float64)) for k, v in weights.items()}
+    n_src = W["wal"].shape[1]
+    h, l, q, u = mixture_features(x, logits, topk_idx, group, n_src, m)
+
+    def bias(name, size):
+        return np.zeros(size) if W.get(name) is None else W[name]
+
+    Pa, Ph, N = W["wah"].shape[0], W["whq"].shape[0], W["wa2"].shape[0]
+    n = h.shape[0]
+    out = {k: np.empty((n, N)) for k in ("probs", "y", "a", "b")}
+    out["alpha"] = np.empty(n)
+    for i in range(n):
+        za = np.maximum(W["wah"] @ h[i] + W["wal"] @ l[i] + bias("ba1", Pa), 0.0)
+        a = W["wa2"] @ za + bias("ba2", N)
+        zh = np.maximum(W["whq"] @ q[i] + W["whu"] @ u[i] + bias("bh1", Ph), 0.0)
+        b = W["wh2"] @ zh + bias("bh2", N)
+        g = W["gh"] @ h[i] + W["gl"] @ l[i] + W["gq"] @ q[i] + W["gu"] @ u[i] + float(W.get("bg") or 0.0)
+        alpha = 1.0 / (1.0 + np.exp(-g))
+        y = alpha * a + (1.0 - alpha) * b
+        e = np.exp(y - y.max())
+        out["probs"][i] = e / e.sum()
+        out["y"][i], out["a"][i], out["b"][i], out["alpha"][i] = y, a, b, alpha
+    return out
 
 
 def coverage_at_k(pred_scores, routed_counts, k: int):

@@ -18,6 +18,8 @@ from ._binding import (  # noqa: F401
     MIRA_MAX_EXPERTS,
     MIRA_MAX_TOPK,
     MiraError,
+    MixtureShape,
+    MixtureWeights,
     MoEArgs,
     MoEShape,
     PredShape,
@@ -29,7 +31,9 @@ from ._binding import (  # noqa: F401
     mira_moe_route,
     mira_pack_experts,
     mira_packed_expert_bytes,
+    mira_mixture_workspace_bytes,
     mira_predict,
+    mira_predict_mixture,
     mira_predict_workspace_bytes,
     mira_profile_enable,
     mira_profile_read,
@@ -49,6 +53,8 @@ EXPORTED_SYMBOLS = (
     "mira_moe_experts",
     "mira_predict_workspace_bytes",
     "mira_predict",
+    "mira_mixture_workspace_bytes",
+    "mira_predict_mixture",
     "mira_stage_expert",
     "mira_set_slot",
     "mira_last_error",

@@ -49,6 +49,19 @@ class _PredShape(ctypes.Structure):
                 ("group", ctypes.c_int32), ("act_dtype", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
+class _MixShape(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("hidden", "n_src", "top_k", "hist_top", "act_hidden",
+                                              "hist_hidden", "n_out", "group", "act_dtype", "reserved")]
+
+
+_MIX_PTRS = ("wah", "wal", "ba1", "wa2", "ba2", "whq", "whu", "bh1", "wh2", "bh2", "gh", "gl", "gq", "gu")
+
+
+class _MixWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in _MIX_PTRS] + [("bg", ctypes.c_float),
+                                                             ("reserved", ctypes.c_int32)]
+
+
 @dataclass
 class MoEShape:
     """mira_shape: C (hidden), R (ffn), E, k, S, activation dtype and flags."""
@@ -76,6 +89,47 @@ class PredShape:
 
     def _c(self) -> _PredShape:
         return _PredShape(self.hidden, self.pred_hidden, self.n_out, self.group, self.act_dtype, 0)
+
+
+@dataclass
+class MixtureShape:
+    """mira_mixture_shape: C, source experts E, k, top-m, head widths, scored experts, group."""
+    hidden: int
+    n_src: int
+    top_k: int
+    hist_top: int
+    act_hidden: int
+    hist_hidden: int
+    n_out: int
+    group: int
+    act_dtype: int = MIRA_BF16
+
+    def _c(self) -> _MixShape:
+        return _MixShape(self.hidden, self.n_src, self.top_k, self.hist_top, self.act_hidden,
+                         self.hist_hidden, self.n_out, self.group, self.act_dtype, 0)
+
+
+@dataclass
+class MixtureWeights:
+    """mira_mixture_weights.  Tensor fields take torch tensors, integer addresses or None."""
+    wah: Any = None
+    wal: Any = None
+    ba1: Any = None
+    wa2: Any = None
+    ba2: Any = None
+    whq: Any = None
+    whu: Any = None
+    bh1: Any = None
+    wh2: Any = None
+    bh2: Any = None
+    gh: Any = None
+    gl: Any = None
+    gq: Any = None
+    gu: Any = None
+    bg: float = 0.0
+
+    def _c(self) -> _MixWeights:
+        return _MixWeights(**{n: _ptr(getattr(self, n)) for n in _MIX_PTRS}, bg=float(self.bg), reserved=0)
 
 
 @dataclass
@@ -161,6 +215,9 @@ def load():
             "mira_predict_workspace_bytes": (sz, [ctypes.POINTER(_PredShape), i32]),
             "mira_predict": (ctypes.c_int, [ctypes.POINTER(_PredShape), vp, i32, vp, vp, vp, vp, vp, vp,
                                             u64, vp]),
+            "mira_mixture_workspace_bytes": (sz, [ctypes.POINTER(_MixShape), i32]),
+            "mira_predict_mixture": (ctypes.c_int, [ctypes.POINTER(_MixShape), ctypes.POINTER(_MixWeights),
+                                                    vp, vp, vp, i32, vp, vp, vp, u64, vp]),
             "mira_stage_expert": (ctypes.c_int, [vp, u64, i32, vp, u64, vp, vp]),
             "mira_set_slot": (ctypes.c_int, [vp, i32, i32, vp]),
             "mira_last_error": (ctypes.c_char_p, []),
@@ -235,6 +292,17 @@ def mira_predict(pshape: PredShape, x, n_tokens: int, w1, b1, w2, b2, scores, wo
     _check(load().mira_predict(ctypes.byref(pshape._c()), _ptr(x), n_tokens, _ptr(w1), _ptr(b1),
                                _ptr(w2), _ptr(b2), _ptr(scores), _ptr(workspace), workspace_bytes,
                                _stream(stream)))
+
+
+def mira_mixture_workspace_bytes(mshape: MixtureShape, n_tokens: int) -> int:
+    return int(load().mira_mixture_workspace_bytes(ctypes.byref(mshape._c()), n_tokens))
+
+
+def mira_predict_mixture(mshape: MixtureShape, weights: MixtureWeights, x, logits, topk_idx,
+                         n_tokens: int, probs, alpha, workspace, workspace_bytes: int, stream=None):
+    _check(load().mira_predict_mixture(ctypes.byref(mshape._c()), ctypes.byref(weights._c()), _ptr(x),
+                                       _ptr(logits), _ptr(topk_idx), n_tokens, _ptr(probs), _ptr(alpha),
+                                       _ptr(workspace), workspace_bytes, _stream(stream)))
 
 
 def mira_stage_expert(slot_pool, slot_stride: int, slot: int, pinned_src, nbytes: int,

@@ -7,6 +7,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdarg>
+#include <cstdint>
 #include <cstdio>
 #include <cstring>
 #include <map>
@@ -430,10 +431,50 @@ int mira_predict(const mira_pred_shape* p, const void* x, int32_t n_tokens, cons
                 n_tokens, p->group);
   if (n_tokens == 0) return ok();
   if (!x || !w1 || !w2 || !scores || !workspace) return fail(MIRA_ERR_ARG, "NULL pointer argument");
+  if (!aligned(w1, 16)) return fail(MIRA_ERR_ALIGN, "w1 must be 16-byte aligned");
   if (!aligned(workspace, 256)) return fail(MIRA_ERR_ALIGN, "workspace must be 256-byte aligned");
   if (workspace_bytes < mira_predict_workspace_bytes(p, n_tokens))
     return fail(MIRA_ERR_WORKSPACE, "predict workspace too small");
   HIP_TRY(mira::launch_predict(*p, x, n_tokens, w1, b1, w2, b2, scores, workspace, stream));
+  return ok();
+}
+
+size_t mira_mixture_workspace_bytes(const mira_mixture_shape* p, int32_t n_tokens) {
+  if (!p || p->group < 1 || p->hidden <= 0 || p->n_src <= 0 || p->act_hidden <= 0 ||
+      p->hist_hidden <= 0 || n_tokens < 0)
+    return 0;
+  return mira::mixture_ws_bytes(n_tokens / p->group, *p);
+}
+
+int mira_predict_mixture(const mira_mixture_shape* p, const mira_mixture_weights* w, const void* x,
+                         const float* logits, const int32_t* topk_idx, int32_t n_tokens,
+                         float* probs, float* alpha, void* workspace, uint64_t workspace_bytes,
+                         hipStream_t stream) {
+  if (!p || !w) return fail(MIRA_ERR_ARG, "mixture shape or weights is NULL");
+  if (p->reserved != 0 || w->reserved != 0) return fail(MIRA_ERR_ARG, "reserved fields must be 0");
+  if (p->hidden <= 0 || p->hidden % 64) return fail(MIRA_ERR_SHAPE, "hidden must be a positive multiple of 64");
+  if (p->n_src < 1 || p->n_src > MIRA_MAX_EXPERTS) return fail(MIRA_ERR_SHAPE, "n_src out of range");
+  if (p->top_k < 1 || p->top_k > MIRA_MAX_TOPK) return fail(MIRA_ERR_SHAPE, "top_k out of range");
+  if (p->hist_top < 1 || p->hist_top > p->n_src) return fail(MIRA_ERR_SHAPE, "hist_top must lie in 1..n_src");
+  if (p->act_hidden < 1 || p->hist_hidden < 1) return fail(MIRA_ERR_SHAPE, "head widths must be >= 1");
+  if (p->n_out < 1 || p->n_out > MIRA_MAX_EXPERTS) return fail(MIRA_ERR_SHAPE, "n_out out of range");
+  if (p->group < 1) return fail(MIRA_ERR_SHAPE, "group must be >= 1");
+  if (p->act_dtype != MIRA_F32 && p->act_dtype != MIRA_BF16) return fail(MIRA_ERR_ARG, "bad act_dtype");
+  if (n_tokens < 0 || n_tokens % p->group)
+    return fail(MIRA_ERR_SHAPE, "n_tokens (%d) must be a non-negative multiple of group (%d)",
+                n_tokens, p->group);
+  if ((int64_t)p->group * p->top_k > INT32_MAX) return fail(MIRA_ERR_SHAPE, "group * top_k overflows");
+  if (n_tokens == 0) return ok();
+  if (!x || !logits || !topk_idx || !probs || !workspace) return fail(MIRA_ERR_ARG, "NULL pointer argument");
+  if (!w->wah || !w->wal || !w->wa2 || !w->whq || !w->whu || !w->wh2 || !w->gh || !w->gl ||
+      !w->gq || !w->gu)
+    return fail(MIRA_ERR_ARG, "NULL weight pointer");
+  if (!aligned(x, 16) || !aligned(w->wah, 16) || !aligned(w->gh, 16))
+    return fail(MIRA_ERR_ALIGN, "x, wah and gh must be 16-byte aligned");
+  if (!aligned(workspace, 256)) return fail(MIRA_ERR_ALIGN, "workspace must be 256-byte aligned");
+  if (workspace_bytes < mira_mixture_workspace_bytes(p, n_tokens))
+    return fail(MIRA_ERR_WORKSPACE, "mixture workspace too small");
+  HIP_TRY(mira::launch_mixture(*p, *w, x, logits, topk_idx, n_tokens, probs, alpha, workspace, stream));
   return ok();
 }
 

@@ -231,6 +231,10 @@ hipError_t launch_pack(int C, int R, int n, int w_dtype, const void* wg, const v
 hipError_t launch_predict(const mira_pred_shape& p, const void* x, int T, const void* w1,
                           const float* b1, const void* w2, const float* b2, float* scores,
                           void* ws, hipStream_t st);
+size_t mixture_ws_bytes(int n_groups, const mira_mixture_shape& p);
+hipError_t launch_mixture(const mira_mixture_shape& p, const mira_mixture_weights& w,
+                          const void* x, const float* logits, const int32_t* topk_idx, int T,
+                          float* probs, float* alpha, void* ws, hipStream_t st);
 hipError_t launch_set_slot(int32_t* table, int expert, int slot, hipStream_t st);
 
 int device_cu_count();

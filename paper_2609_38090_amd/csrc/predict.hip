@@ -2,6 +2,7 @@
 // layer l's hidden states, then a two-layer MLP (ReLU, sigmoid) scoring the
 // experts of layer l+2.  Three small kernels, fp32 accumulation.
 #include "device_util.h"
+#include "head_dev.h"
 #include "mira_internal.h"
 
 namespace mira {
@@ -13,12 +14,14 @@ __global__ __launch_bounds__(256) void pred_pool_kernel(const ActT* __restrict__
   const int i = blockIdx.y;
   const int c = blockIdx.x * 256 + threadIdx.x;
   if (c >= C) return;
-  float s = 0.f;
-  for (int r = 0; r < group; ++r) s += load_act(x, (size_t)(i * group + r) * C + c);
+  const float s = head_col_sum(group, [&](int r) { return load_act(x, (size_t)(i * group + r) * C + c); });
   f[(size_t)i * C + c] = s / (float)group;
 }
 
-// z[i][p] = max(0, sum_c W1[p][c] f[i][c] + b1[p]); one wave per row p
+// z[i][p] = max(0, sum_c W1[p][c] f[i][c] + b1[p]); one wave per row p, which
+// sweeps the row once per kPredGroups pooled rows.
+constexpr int kPredGroups = 4;
+
 __global__ __launch_bounds__(256) void pred_layer1_kernel(const uint16_t* __restrict__ w1,
                                                           const float* __restrict__ b1,
                                                           const float* __restrict__ f, int C, int P,
@@ -26,12 +29,20 @@ __global__ __launch_bounds__(256) void pred_layer1_kernel(const uint16_t* __rest
   const int p = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (p >= P) return;
   const uint16_t* wr = w1 + (size_t)p * C;
-  for (int i = 0; i < n; ++i) {
-    const float* fi = f + (size_t)i * C;
-    float s = 0.f;
-    for (int c = lane; c < C; c += 64) s = fmaf(bf16_to_f32(wr[c]), fi[c], s);
-    s = wave_sum(s);
-    if (lane == 0) z[(size_t)i * P + p] = fmaxf(s + (b1 ? b1[p] : 0.f), 0.f);
+  const float bias = b1 ? b1[p] : 0.f;
+  for (int i0 = 0; i0 < n; i0 += kPredGroups) {
+    const int ng = min(kPredGroups, n - i0);
+    float acc[kPredGroups];
+#pragma unroll
+    for (int j = 0; j < kPredGroups; ++j) acc[j] = 0.f;
+    head_row_dot(wr, f + (size_t)i0 * C, C, ng, lane, acc);
+#pragma unroll
+    for (int j = 0; j < kPredGroups; ++j) {
+      if (j < ng) {
+        const float s = wave_sum(acc[j]);
+        if (lane == 0) z[(size_t)(i0 + j) * P + p] = fmaxf(s + bias, 0.f);
+      }
+    }
   }
 }
 
@@ -45,9 +56,7 @@ __global__ __launch_bounds__(256) void pred_layer2_kernel(const uint16_t* __rest
   const int i = q / E, e = q - i * E;
   const uint16_t* wr = w2 + (size_t)e * P;
   const float* zi = z + (size_t)i * P;
-  float s = 0.f;
-  for (int p = lane; p < P; p += 64) s = fmaf(bf16_to_f32(wr[p]), zi[p], s);
-  s = wave_sum(s);
+  const float s = wave_sum(head_lane_dot(wr, zi, P, lane));
   if (lane == 0) scores[(size_t)i * E + e] = 1.f / (1.f + expf(-(s + (b2 ? b2[e] : 0.f))));
 }
 

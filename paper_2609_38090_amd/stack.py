@@ -5,8 +5,9 @@ Paper sections IV-C (HOT and STAGE regions of the expert cache), IV-D
 layer l+2's experts on a copy stream) and IV-F (the staging copies overlap the
 compute stream).  This module is the host-side bookkeeping of a decode step
 through L layers; every byte still moves through the library:
-mira_moe_route / mira_moe_experts run a layer, mira_predict scores layer
-l+2's experts, mira_stage_expert copies a packed expert from pinned host
+mira_moe_route / mira_moe_experts run a layer, mira_predict (the MLP head) or
+mira_predict_mixture (the MixtureHead, fed by the layer's router logits and
+selections) scores layer l+2's experts, mira_stage_expert copies a packed expert from pinned host
 memory into a slot on the copy stream, and mira_set_slot updates a layer's
 slot table in stream order.
 
@@ -74,7 +75,8 @@ class LayerData:
     bias: torch.Tensor | None   # [E] fp32
     hot: list                   # experts resident in HOT slots at the start
     host: dict = field(default_factory=dict)  # expert -> pinned packed blob (experts not HOT at the start)
-    pred: tuple | None = None   # (w1, b1, w2, b2) of the head scoring layer l+2
+    pred: object = None         # head scoring layer l+2: (w1, b1, w2, b2) of the MLP head,
+                                # or mira.MixtureWeights of a MixtureHead
 
 
 class ExpertStack:
@@ -82,7 +84,7 @@ class ExpertStack:
     expert of every layer, then n_stage STAGE slots."""
 
     def __init__(self, shape: mira.MoEShape, tokens: int, layers: list, stride: int,
-                 n_stage: int, pred_shape: mira.PredShape | None = None, device="cuda",
+                 n_stage: int, pred_shape=None, device="cuda",
                  vram_mode: str = "large", rebalancer: Rebalancer | None = None):
         if vram_mode not in ("small", "large"):
             raise ValueError("vram_mode must be 'small' or 'large'")
@@ -123,22 +125,51 @@ class ExpertStack:
         self.counts = torch.zeros((self.E + shape.n_shared,), dtype=torch.int32, device=device)
         self.counts_h = torch.zeros_like(self.counts, device="cpu").pin_memory()
         self.status = torch.zeros((1,), dtype=torch.int32, device=device)
-        self.pred_shape = pred_shape
-        if pred_shape is not None:
-            self.pws = torch.empty(mira.mira_predict_workspace_bytes(pred_shape, tokens), dtype=torch.uint8,
-                                   device=device)
-            self.scores = torch.empty((tokens // pred_shape.group, pred_shape.n_out), dtype=torch.float32,
-                                      device=device)
-            self.scores_h = torch.zeros(self.scores.shape, dtype=torch.float32).pin_memory()
+        self.pred_shape, self.mixture, self.logits = None, False, None
+        self.set_predictor(pred_shape)
         self.compute = torch.cuda.current_stream(device)
         self.copy = torch.cuda.Stream(device)  # default priority
+        self.side = torch.cuda.Stream(device)  # predictor heads, beside the experts (default priority)
+
+    def set_predictor(self, pred_shape, heads=None):
+        """Select the predictor head: a mira.PredShape (MLP heads) or a
+        mira.MixtureShape (MixtureHeads, which also read the router logits).
+        heads, if given, replaces LayerData.pred of every layer."""
+        if heads is not None:
+            for ld, h in zip(self.layers, heads):
+                ld.pred = h
+        self.pred_shape = pred_shape
+        self.mixture = isinstance(pred_shape, mira.MixtureShape)
+        self.logits = (torch.empty((self.T, self.E), dtype=torch.float32, device=self.device)
+                       if self.mixture else None)
+        if pred_shape is not None:
+            ws = (mira.mira_mixture_workspace_bytes(pred_shape, self.T) if self.mixture
+                  else mira.mira_predict_workspace_bytes(pred_shape, self.T))
+            self.pws = torch.empty(max(ws, 256), dtype=torch.uint8, device=self.device)
+            self.scores = torch.empty((self.T // pred_shape.group, pred_shape.n_out), dtype=torch.float32,
+                                      device=self.device)
+            self.scores_h = torch.zeros(self.scores.shape, dtype=torch.float32).pin_memory()
+
+    def _predict(self, l: int):
+        """Queue layer l's predictor head and the copy of its scores to the
+        host on the side stream."""
+        ld = self.layers[l]
+        if self.mixture:
+            mira.mira_predict_mixture(self.pred_shape, ld.pred, ld.x, self.logits, self.idx, self.T,
+                                      self.scores, None, self.pws, self.pws.numel(), self.side)
+        else:
+            w1p, b1p, w2p, b2p = ld.pred
+            mira.mira_predict(self.pred_shape, ld.x, self.T, w1p, b1p, w2p, b2p, self.scores, self.pws,
+                              self.pws.numel(), self.side)
+        with torch.cuda.stream(self.side):
+            self.scores_h.copy_(self.scores, non_blocking=True)
 
     def args(self, l: int) -> mira.MoEArgs:
         ld = self.layers[l]
         return mira.MoEArgs(x=ld.x, n_tokens=self.T, n_slots=self.n_slots, w_router=ld.w_router,
                             router_bias=ld.bias, slot_table=self.tables[l], slot_pool=self.pool,
                             slot_stride=self.stride, out=self.out, topk_idx=self.idx,
-                            expert_counts=self.counts, status=self.status, workspace=self.ws,
+                            logits=self.logits, expert_counts=self.counts, status=self.status, workspace=self.ws,
                             workspace_bytes=self.ws.numel())
 
     def hot_set(self, l: int) -> set:
@@ -250,6 +281,15 @@ class ExpertStack:
             a = self.args(l)
             tel = self.telemetry[l]
             mira.mira_moe_route(self.shape, a, self.compute)
+            tgt = l + 2
+            predicting = mode == "predict" and tgt < L
+            if predicting:
+                # the head for layer l+2 needs only layer l's input and routing:
+                # it runs on the side stream while layer l's experts run
+                routed = torch.cuda.Event()
+                routed.record(self.compute)
+                self.side.wait_event(routed)
+                self._predict(l)
             self.counts_h.copy_(self.counts, non_blocking=True)
             self.compute.synchronize()
             cnt = [int(self.counts_h[e]) for e in range(self.E)]
@@ -282,14 +322,9 @@ class ExpertStack:
                     if self.vram_mode == "small":
                         self.held[i], self.ready[i] = None, None
             # prefetch controller: experts of layer l+2
-            tgt = l + 2
             if tgt < L and mode != "demand":
-                if mode == "predict":
-                    w1p, b1p, w2p, b2p = self.layers[l].pred
-                    mira.mira_predict(self.pred_shape, self.layers[l].x, self.T, w1p, b1p, w2p, b2p,
-                                      self.scores, self.pws, self.pws.numel(), self.compute)
-                    self.scores_h.copy_(self.scores, non_blocking=True)
-                    self.compute.synchronize()
+                if predicting:
+                    self.side.synchronize()
                     s = self.scores_h.sum(dim=0)
                     want = sorted(range(self.E), key=lambda e: (-float(s[e]), e))[:stage_per_layer]
                 else:  # oracle

@@ -140,3 +140,33 @@ def test_host_pack_fine_grained_expert_slice():
     wg, wu, wd = (t.numpy()[None] for t in expert_weights(cfg, 0, 5))
     got = _host_pack(cfg.C, cfg.R, wg, wu, wd)
     assert np.array_equal(got[0], oracle.pack_expert(wg[0], wu[0], wd[0]))
+
+
+def test_mixture_head_argument_checks():
+    shape = dict(hidden=64, n_src=4, top_k=2, hist_top=2, act_hidden=8, hist_hidden=8, n_out=4, group=2,
+                 act_dtype=mira.MIRA_F32)
+    good = mira.MixtureShape(**shape)
+    ws = mira.mira_mixture_workspace_bytes(good, 4)
+    assert ws > 0 and ws % 256 == 0
+    assert mira.mira_mixture_workspace_bytes(good, 8) >= ws
+    w = mira.MixtureWeights(**{n: 0x1000 * (i + 1) for i, n in enumerate(
+        ("wah", "wal", "ba1", "wa2", "ba2", "whq", "whu", "bh1", "wh2", "bh2", "gh", "gl", "gq", "gu"))})
+    args = dict(x=0x100000, logits=0x200000, topk_idx=0x300000, n_tokens=4, probs=0x400000, alpha=None,
+                workspace=0x500000, workspace_bytes=ws)
+    mira.mira_predict_mixture(good, w, **dict(args, n_tokens=0), stream=1)   # no-op
+    for change, code in [(dict(hidden=100), -2), (dict(n_src=0), -2), (dict(n_src=257), -2),
+                         (dict(top_k=17), -2), (dict(hist_top=5), -2), (dict(hist_top=0), -2),
+                         (dict(act_hidden=0), -2), (dict(n_out=300), -2), (dict(group=0), -2),
+                         (dict(act_dtype=5), -1)]:
+        with pytest.raises(mira.MiraError) as ei:
+            mira.mira_predict_mixture(mira.MixtureShape(**dict(shape, **change)), w, **args, stream=1)
+        assert ei.value.code == code, change
+    for change, code in [(dict(n_tokens=3), -2), (dict(x=None), -1), (dict(x=0x100008), -3),
+                         (dict(workspace=0x500010), -3), (dict(workspace_bytes=ws - 256), -4)]:
+        with pytest.raises(mira.MiraError) as ei:
+            mira.mira_predict_mixture(good, w, **dict(args, **change), stream=1)
+        assert ei.value.code == code, change
+    for field, val in (("gq", None), ("wah", 0x1008)):
+        bad = mira.MixtureWeights(**{**w.__dict__, field: val})
+        with pytest.raises(mira.MiraError):
+            mira.mira_predict_mixture(good, bad, **args, stream=1)

@@ -8,27 +8,39 @@ import torch
 
 import oracle
 from gpu_layer import EPS, assert_ffn_close
-from mira_inputs import (MoEConfig, activations, expert_weights, predictor_weights, resident_experts,
-                         router_bias, router_weights)
+from mira_inputs import (MoEConfig, activations, expert_weights, mixture_weights, predictor_weights,
+                         resident_experts, router_bias, router_weights)
 
 pytestmark = pytest.mark.gpu
+
+MIX_PA, MIX_PH = 48, 16  # MixtureHead widths of the small stack
 
 SMALL_STACK = MoEConfig("small_stack", 104, T=8, C=128, E=8, k=2, R=192, zipf_s=1.2, layers=5, resident=4,
                         pred_hidden=32, pred_group=8)
 
 
-def build(mira, cfg, n_stage, hot=None, bias=None, host_all=False, rebalancer=None):
+def _head(mira, cfg, l, head):
+    if l + 2 >= cfg.layers:
+        return None
+    if head == "mlp":
+        return tuple(t.cuda() for t in predictor_weights(cfg, l, "cpu"))
+    W = mixture_weights(cfg, l, MIX_PA, MIX_PH)
+    return mira.MixtureWeights(**{k: v.cuda() for k, v in W.items() if torch.is_tensor(v)}, bg=W["bg"])
+
+
+def build(mira, cfg, n_stage, hot=None, bias=None, host_all=False, rebalancer=None, head="mlp"):
     from paper_2609_38090_amd.stack import ExpertStack, LayerData
     stride = mira.mira_packed_expert_bytes(cfg.C, cfg.R)
     layers, blobs = [], {}
     for l in range(cfg.layers):
         b = router_bias(cfg, l) if bias is None else bias(l)
-        pred = tuple(t.cuda() for t in predictor_weights(cfg, l, "cpu")) if l + 2 < cfg.layers else None
+        pred = _head(mira, cfg, l, head)
         layers.append(LayerData(x=activations(cfg, l, "cuda"), w_router=router_weights(cfg, l, "cuda"),
                                 bias=None if b is None else b.cuda(),
                                 hot=resident_experts(cfg, l) if hot is None else hot(l), pred=pred))
     shape = mira.MoEShape(cfg.C, cfg.R, cfg.E, cfg.k, cfg.S, mira.MIRA_BF16, 0)
-    ps = mira.PredShape(cfg.C, cfg.pred_hidden, cfg.E, cfg.pred_group, mira.MIRA_BF16)
+    ps = (mira.PredShape(cfg.C, cfg.pred_hidden, cfg.E, cfg.pred_group, mira.MIRA_BF16) if head == "mlp" else
+          mira.MixtureShape(cfg.C, cfg.E, cfg.k, cfg.k, MIX_PA, MIX_PH, cfg.E, cfg.pred_group, mira.MIRA_BF16))
     st = ExpertStack(shape, cfg.T, layers, stride, n_stage=n_stage, pred_shape=ps, rebalancer=rebalancer)
     pack_shape = mira.MoEShape(cfg.C, cfg.R, 1, 1)
     for l, ld in enumerate(layers):
@@ -125,3 +137,48 @@ def test_rebalancer_tracks_drift_without_changing_outputs(mira):
     got_fixed = sum(len(fixed.hot_set(l) & last[l]) for l in range(cfg.layers))
     got_moving = sum(len(moving.hot_set(l) & last[l]) for l in range(cfg.layers))
     assert got_moving > got_fixed, (got_moving, got_fixed)
+
+
+def test_stack_with_mixture_head_stages_its_top_experts(mira):
+    """Predictive staging driven by the MixtureHead: outputs stay bit-identical
+    to demand fetching, and the experts requested for layer l+2 are the two with
+    the largest MixtureHead probability summed over the step's groups (oracle
+    on the layer's routing record; checked where the ranking has a clear gap)."""
+    cfg = SMALL_STACK
+    st, _ = build(mira, cfg, 8, head="mixture")
+    dem, _ = run(st, "demand")
+    st.reset_stage()
+    requested = []
+    orig = st._stage
+
+    def spy(tgt, e, *a, **kw):
+        if not a[1]:  # a prefetch, not a demand copy
+            requested.append((tgt, e))
+        return orig(tgt, e, *a, **kw)
+
+    st._stage = spy
+    routing = {}
+
+    def grab(l, out):
+        routing[l] = (st.logits.cpu().numpy().copy(), st.idx.cpu().numpy().copy(), out.clone())
+
+    stats = st.step("predict", on_layer=grab)
+    torch.cuda.synchronize()
+    for l in range(cfg.layers):
+        assert np.array_equal(routing[l][2].cpu().numpy(), dem[l]), l
+    assert stats.prefetches + stats.prefetch_cached + stats.prefetch_declined == 2 * (cfg.layers - 2)
+    checked = 0
+    for l in range(cfg.layers - 2):
+        W = mixture_weights(cfg, l, MIX_PA, MIX_PH)
+        W64 = {k: (v.double().numpy() if torch.is_tensor(v) else v) for k, v in W.items()}
+        x = st.layers[l].x.float().cpu().numpy().astype(np.float64)
+        logits, idx, _ = routing[l]
+        ref = oracle.mixture_head(x, logits.astype(np.float64), idx, cfg.pred_group, cfg.k, W64)["probs"].sum(0)
+        order = np.argsort(-ref, kind="stable")
+        if ref[order[1]] - ref[order[2]] < 1e-4:
+            continue
+        want = set(order[:2].tolist())
+        got = {e for (t, e) in requested if t == l + 2}
+        assert got == want - st.hot_set(l + 2), (l, got, want)
+        checked += 1
+    assert checked > 0
