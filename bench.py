@@ -491,10 +491,10 @@ def run_stack(args, cfg):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+        print(json.dumps({"error": "the benchmark runs on one GPU only; --gpus must be 1",
                           "n_gpus": args.gpus}))
-        print("bench.py measures the single-GPU MoE expert step; multi-GPU runs are not part "
-              "of this build (see the sharding notes in DESIGN.md).", file=sys.stderr)
+        print("bench.py measures the MoE expert step on a single GPU; the library has no "
+              "multi-GPU path (no sharding, no collectives).", file=sys.stderr)
         return 2
 
     if args.source_hash:

@@ -49,7 +49,7 @@ typedef enum mira_status {
   MIRA_ERR_ALIGN = -3,      /* a pointer or stride breaks the stated alignment */
   MIRA_ERR_WORKSPACE = -4,  /* workspace missing or smaller than mira_workspace_bytes() */
   MIRA_ERR_HIP = -5,        /* a HIP runtime call failed; the message names it */
-  MIRA_ERR_UNSUPPORTED = -6 /* valid request this build does not implement */
+  MIRA_ERR_UNSUPPORTED = -6 /* valid request the library does not implement */
 } mira_status;
 
 /* ---- element types ------------------------------------------------------ */
@@ -71,7 +71,7 @@ typedef enum mira_dtype {
 /* Without a FORCE flag, calls with n_tokens <= this use the decode kernels. */
 #define MIRA_DECODE_MAX_TOKENS 16
 
-/* Size limits of this build. */
+/* Size limits of the library. */
 #define MIRA_MAX_EXPERTS 256 /* n_experts + n_shared */
 #define MIRA_MAX_TOPK 16
 
