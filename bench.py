@@ -84,6 +84,9 @@ def parse():
                    help="beam stack: steps of the drifting-popularity HOT rebalancing run (0 = skip)")
     p.add_argument("--source-hash", action="store_true",
                    help="print the source hashes the traffic table is keyed on and exit")
+    p.add_argument("--scale-bench", action="store_true",
+                   help="instead of the MoE step, time staging only the scale metadata of experts: "
+                        "one shared scale vector per expert against three per-matrix vectors")
     p.add_argument("--copy-bytes", type=int, default=0,
                    help="instead of the MoE step, time a plain device-to-device copy of this many "
                         "bytes (the reference kernel for scaling the FETCH_SIZE/WRITE_SIZE counters)")
@@ -105,6 +108,58 @@ def copy_reference(nbytes, steps):
     print(json.dumps({"copy_bytes": nbytes, "steps": steps, "ms_per_copy": round(dt * 1e3, 4),
                       "gbs_read_plus_write": round(2 * nbytes / dt / 1e9, 1)}), flush=True)
     return 0
+
+
+# Expert shapes of the scale-only staging microbenchmark: hidden C, expert ffn
+# R and the experts of one layer (routed + shared) staged together.
+SCALE_SHAPES = {
+    "mixtral_8x7b": dict(C=4096, R=14336, experts=8),
+    "mixtral_8x22b": dict(C=6144, R=16384, experts=8),
+    "deepseek_v2_lite": dict(C=2048, R=1408, experts=66),
+}
+
+
+def scale_bench(reps=200):
+    """Staging of scale metadata only (section IV-B): the shared format moves
+    one bf16 vector of R scales per expert in one copy; per-matrix per-row
+    INT8 moves the gate and up row scales (R each) and the down row scales
+    (C) in three copies.  Every copy is a mira_stage_expert call (pinned host
+    -> device on one stream); the time of a whole layer's experts is taken
+    between two events, median over reps."""
+    import torch
+    import paper_2609_38090_amd as mira
+
+    mira.load()
+    st = torch.cuda.Stream()
+    out = {}
+    for name, sh in SCALE_SHAPES.items():
+        C, R, n = sh["C"], sh["R"], sh["experts"]
+        layouts = {"shared": [2 * R], "per_matrix": [2 * R, 2 * R, 2 * C]}
+        res = {}
+        for kind, sizes in layouts.items():
+            src = [torch.ones(n * b, dtype=torch.uint8).pin_memory() for b in sizes]
+            dst = [torch.empty(n * b, dtype=torch.uint8, device="cuda") for b in sizes]
+            times = []
+            for it in range(reps + 10):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(st)
+                for e in range(n):
+                    for s_, d_, b in zip(src, dst, sizes):
+                        mira.mira_stage_expert(d_, b, e, s_[e * b:].data_ptr(), b, st, None)
+                e1.record(st)
+                e1.synchronize()
+                if it >= 10:
+                    times.append(e0.elapsed_time(e1) * 1e3)
+            times.sort()
+            med = times[len(times) // 2]
+            res[kind] = dict(copies_per_expert=len(sizes), bytes_per_expert=sum(sizes),
+                             us_per_layer=round(med, 2), us_per_expert=round(med / n, 3))
+        res["latency_ratio"] = round(res["per_matrix"]["us_per_layer"] / res["shared"]["us_per_layer"], 2)
+        res["bytes_ratio"] = round((4 * R + 2 * C) / (2 * R), 2)
+        out[name] = dict(hidden=C, ffn=R, experts=n, **res)
+    line = {"microbenchmark": "scale-only staging, pinned host -> device", "reps": reps, "shapes": out}
+    print(json.dumps(line), flush=True)
+    return line
 
 
 def build_copies(cfg, n_copies):
@@ -496,6 +551,10 @@ def main():
         print("bench.py measures the MoE expert step on a single GPU; the library has no "
               "multi-GPU path (no sharding, no collectives).", file=sys.stderr)
         return 2
+
+    if args.scale_bench:
+        scale_bench()
+        return 0
 
     if args.source_hash:
         print(json.dumps({f"{k[0]}/{k[1]}": source_hash(v["sources"]) for k, v in TRAFFIC.items()}))

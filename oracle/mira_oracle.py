@@ -31,6 +31,20 @@ notes of the repository):
   descending with the lower expert index winning ties; combine weights are a
   softmax over the k selected logits (renormalised top-k); shared experts, if
   any, are added with weight 1.
+* INT4 variant (the workload's 4-bit, group-64, fp16-scale format; the paper
+  reports INT4 only as a quality point, Table I): per row and group of 64
+  consecutive columns, alpha = max |w| over the group (exact), the fp32 value
+  fl32(max(alpha, eps) / 7) is rounded to fp16 (nearest, ties to even; a
+  result of zero becomes the smallest positive fp16 2^-24, an overflow the
+  largest finite 65504), and q = clamp(round_half_even(fl32(w / s)), -7, 7)
+  against that stored s.  gate, up and down each carry their own scales.
+* INT4 byte layout: each matrix [rows][K] is cut into 16 x 64 tiles stored
+  like the INT8 tiles (tile-rows in order, column blocks in order); a tile is
+  544 bytes: 512 bytes of nibbles, then the 16 fp16 scales of its rows for
+  its column block.  Run g*16 + i (8 bytes) holds row i, columns
+  16g .. 16g+15: byte b (0..7) carries column 16g + 8*(b//4) + (b%4) in its
+  high nibble and column 16g + 8*(b//4) + 4 + (b%4) in its low nibble, each
+  nibble the two's complement of q.
 * Permutation: (token, slot) pairs p = t*k + j are grouped by expert with a
   stable counting sort; shared-expert pairs follow the routed ones, in token
   order.
@@ -64,6 +78,13 @@ __all__ = [
     "pack_expert",
     "unpack_expert",
     "dequantize_expert",
+    "INT4_TILE_BYTES",
+    "packed_expert_bytes_int4",
+    "int4_tile_order",
+    "int4_untile_order",
+    "pack_expert_int4",
+    "unpack_expert_int4",
+    "dequantize_expert_int4",
     "router_logits",
     "topk_select",
     "near_tie_tokens",
@@ -217,6 +238,114 @@ def dequantize_expert(blob, C: int, R: int):
 
 
 # ----------------------------------------------------------------------------
+# INT4 variant: group-64 scales in fp16 (Table I's INT4 point)
+# ----------------------------------------------------------------------------
+
+INT4_TILE_BYTES = 544   # 16 x 64 nibbles (512 bytes) + 16 fp16 row scales
+INT4_QMAX = 7
+
+
+def packed_expert_bytes_int4(C: int, R: int) -> int:
+    """Bytes of one INT4 expert: 3 * (R/16) * (C/64) tiles of 544 bytes, padded to 256."""
+    n = 3 * (R // 16) * (C // 64) * INT4_TILE_BYTES
+    return (n + BLOB_ALIGN - 1) // BLOB_ALIGN * BLOB_ALIGN
+
+
+def _int4_group_scales(w, eps):
+    """fp16 scale per row and 64-column group (see the module notes)."""
+    rows, K = w.shape
+    alpha = np.abs(w).reshape(rows, K // 64, 64).max(axis=2).astype(np.float32)
+    s32 = (np.maximum(alpha, np.float32(eps)) / np.float32(INT4_QMAX)).astype(np.float32)
+    with np.errstate(over="ignore"):
+        s16 = s32.astype(np.float16)             # round to nearest, ties to even
+    s16 = np.where(np.isinf(s16), np.float16(65504.0), s16)
+    s16 = np.where(s16 == 0, np.float16(2.0 ** -24), s16)
+    return s16.astype(np.float16)
+
+
+def _quantize_int4(w, s16):
+    """q = clamp(round_half_even(fl32(w / s)), -7, 7) per group of 64 columns."""
+    rows, K = w.shape
+    s = s16.astype(np.float32)[:, :, None]
+    quot = (w.reshape(rows, K // 64, 64) / s).astype(np.float32)
+    q = np.clip(np.rint(quot), -INT4_QMAX, INT4_QMAX)
+    return q.reshape(rows, K).astype(np.int8)
+
+
+def int4_tile_order(q, s16):
+    """Bytes of one INT4 matrix q [rows][K] with its scales s16 [rows][K/64]."""
+    q = np.asarray(q)
+    rows, K = q.shape
+    if rows % 16 or K % 64:
+        raise ValueError("tiled layout needs rows % 16 == 0 and K % 64 == 0")
+    nib = (q.astype(np.int16) & 0xF).astype(np.uint8)
+    # column inside a 64-block = 16g + 8h + 4p + j; p = 0 high nibble, 1 low nibble
+    t = nib.reshape(rows // 16, 16, K // 64, 4, 2, 2, 4)          # [tr][i][blk][g][h][p][j]
+    byte = (t[:, :, :, :, :, 0, :] << 4) | t[:, :, :, :, :, 1, :]  # [tr][i][blk][g][h][j]
+    byte = byte.transpose(0, 2, 3, 1, 4, 5).reshape(rows // 16, K // 64, 512)
+    sc = np.asarray(s16, dtype="<f2").reshape(rows // 16, 16, K // 64).transpose(0, 2, 1)
+    sc = np.ascontiguousarray(sc).view(np.uint8).reshape(rows // 16, K // 64, 32)
+    return np.concatenate([byte.astype(np.uint8), sc], axis=2).reshape(-1)
+
+
+def int4_untile_order(flat, rows, K):
+    """Inverse of int4_tile_order: (q [rows][K] int8, s16 [rows][K/64])."""
+    t = np.asarray(flat, dtype=np.uint8).reshape(rows // 16, K // 64, INT4_TILE_BYTES)
+    b = t[:, :, :512].reshape(rows // 16, K // 64, 4, 16, 2, 4)   # [tr][blk][g][i][h][j]
+    hi = (b >> 4).astype(np.int16)
+    lo = (b & 0xF).astype(np.int16)
+    hi = np.where(hi >= 8, hi - 16, hi)
+    lo = np.where(lo >= 8, lo - 16, lo)
+    q = np.stack([hi, lo], axis=5)                                 # [tr][blk][g][i][h][p][j]
+    q = q.transpose(0, 3, 1, 2, 4, 5, 6).reshape(rows, K).astype(np.int8)
+    sc = np.ascontiguousarray(t[:, :, 512:]).view("<f2").reshape(rows // 16, K // 64, 16)
+    s16 = sc.transpose(0, 2, 1).reshape(rows, K // 64).astype(np.float16)
+    return q, s16
+
+
+def pack_expert_int4(w_gate, w_up, w_down, eps=1e-8):
+    """Pack one expert in the INT4 variant (uint8 array of packed_expert_bytes_int4(C, R))."""
+    w_gate = np.asarray(w_gate, dtype=np.float32)
+    w_up = np.asarray(w_up, dtype=np.float32)
+    w_down = np.asarray(w_down, dtype=np.float32)
+    R, C = w_gate.shape
+    if w_up.shape != (R, C) or w_down.shape != (C, R):
+        raise ValueError("expected gate/up [R][C] and down [C][R]")
+    if R % 64 or C % 64:
+        raise ValueError("C and R must be multiples of 64")
+    if not (np.all(np.isfinite(w_gate)) and np.all(np.isfinite(w_up)) and np.all(np.isfinite(w_down))):
+        raise ValueError("non-finite weights are out of contract")
+    blob = np.zeros(packed_expert_bytes_int4(C, R), dtype=np.uint8)
+    o = 0
+    for w in (w_gate, w_up, w_down):
+        s16 = _int4_group_scales(w, eps)
+        part = int4_tile_order(_quantize_int4(w, s16), s16)
+        blob[o:o + part.size] = part
+        o += part.size
+    return blob
+
+
+def unpack_expert_int4(blob, C: int, R: int):
+    """((q_gate, s_gate), (q_up, s_up), (q_down, s_down)) of an INT4 blob."""
+    blob = np.asarray(blob, dtype=np.uint8)
+    n = (R // 16) * (C // 64) * INT4_TILE_BYTES
+    if blob.size < 3 * n:
+        raise ValueError("blob too small for the given shape")
+    return (int4_untile_order(blob[0:n], R, C), int4_untile_order(blob[n:2 * n], R, C),
+            int4_untile_order(blob[2 * n:3 * n], C, R))
+
+
+def dequantize_expert_int4(blob, C: int, R: int):
+    """W_hat = s[row, group] * q (fp64, exact) for the three matrices."""
+    out = []
+    for q, s16 in unpack_expert_int4(blob, C, R):
+        rows, K = q.shape
+        s = np.repeat(s16.astype(np.float64), 64, axis=1)
+        out.append(q.astype(np.float64) * s)
+    return tuple(out)
+
+
+# ----------------------------------------------------------------------------
 # a1-a3: router, top-k, combine weights, permutation (section II-A)
 # ----------------------------------------------------------------------------
 
@@ -327,9 +456,15 @@ def _silu(g):
     return g / (1.0 + np.exp(-g))
 
 
-def expert_ffn(blob, x_rows, C: int, R: int):
-    """SwiGLU expert on dequantized weights: y = Wd (silu(Wg x) * (Wu x)), fp64."""
-    wg, wu, wd = dequantize_expert(blob, C, R)
+def expert_ffn(blob, x_rows, C: int, R: int, fmt: str = "int8"):
+    """SwiGLU expert on dequantized weights: y = Wd (silu(Wg x) * (Wu x)), fp64.
+    fmt: "int8" (the paper's shared-scale format) or "int4" (group-64 variant)."""
+    if fmt == "int8":
+        wg, wu, wd = dequantize_expert(blob, C, R)
+    elif fmt == "int4":
+        wg, wu, wd = dequantize_expert_int4(blob, C, R)
+    else:
+        raise ValueError(f"unknown format {fmt!r}")
     x = np.asarray(x_rows, dtype=np.float64).reshape(-1, C)
     g = x @ wg.T
     u = x @ wu.T
@@ -338,14 +473,15 @@ def expert_ffn(blob, x_rows, C: int, R: int):
 
 
 def moe_forward(x, w_router, bias, blobs, k: int, C: int, R: int,
-                shared_blobs=(), norm_topk: bool = True, idx=None, tokens=None):
+                shared_blobs=(), norm_topk: bool = True, idx=None, tokens=None, fmt: str = "int8"):
     """One MoE layer (section II-A) over experts in the packed format.
 
     blobs[e] is routed expert e's blob, shared_blobs[s] shared expert s's.
     idx, if given, replaces the oracle's own top-k (used to evaluate an
     alternative, equally valid selection on near-tie tokens).  tokens, if
     given, restricts the computation to those token rows (outputs in that
-    order).  Returns out [T'][C] fp64 plus the routing intermediates.
+    order).  fmt names the blobs' format ("int8" or "int4").  Returns out
+    [T'][C] fp64 plus the routing intermediates.
     """
     x = np.asarray(x, dtype=np.float64)
     logits = router_logits(x, w_router, bias)
@@ -366,11 +502,11 @@ def moe_forward(x, w_router, bias, blobs, k: int, C: int, R: int,
         if not sel_t:
             continue
         xs = x[rows[sel_t]]
-        y = expert_ffn(blobs[e], xs, C, R)
+        y = expert_ffn(blobs[e], xs, C, R, fmt)
         for n, (i, j) in enumerate(zip(sel_t, sel_j)):
             out[i] += w[rows[i], j] * y[n]
     for sb in shared_blobs:
-        out += expert_ffn(sb, x[rows], C, R)
+        out += expert_ffn(sb, x[rows], C, R, fmt)
     return {"out": out, "logits": logits, "idx": idx, "w": w}
 
 
