@@ -75,6 +75,9 @@ def parse():
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--workload", default="mixtral_decode",
                    choices=["tiny", "mixtral_decode", "mixtral_prefill", "fine_grained", "beam_stack"])
+    p.add_argument("--format", default="int8", choices=["int8", "int4"],
+                   help="expert format: the paper's shared-scale INT8, or the INT4 variant "
+                        "(group-64 fp16 scales; decode workloads only)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-profile", action="store_true", help="skip the per-kernel HIP-event timing")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample")
@@ -162,15 +165,26 @@ def scale_bench(reps=200):
     return line
 
 
-def build_copies(cfg, n_copies):
+def expert_stride(cfg, fmt):
+    import paper_2609_38090_amd as mira
+    return (mira.mira_packed_expert_bytes_int4(cfg.C, cfg.R) if fmt == "int4"
+            else mira.mira_packed_expert_bytes(cfg.C, cfg.R))
+
+
+def format_flag(fmt):
+    import paper_2609_38090_amd as mira
+    return mira.MIRA_FLAG_INT4 if fmt == "int4" else 0
+
+
+def build_copies(cfg, n_copies, fmt="int8"):
     """n_copies packed copies of the layer (different seeded weights per copy)."""
     import torch
     import paper_2609_38090_amd as mira
     from mira_inputs import activations, expert_weights, router_bias, router_weights
 
-    stride = mira.mira_packed_expert_bytes(cfg.C, cfg.R)
+    stride = expert_stride(cfg, fmt)
     act = mira.MIRA_F32 if cfg.act == "f32" else mira.MIRA_BF16
-    pack_shape = mira.MoEShape(cfg.C, cfg.R, 1, 1)
+    pack_shape = mira.MoEShape(cfg.C, cfg.R, 1, 1, flags=format_flag(fmt))
     copies = []
     for l in range(n_copies):
         pool = torch.empty(cfg.G * stride, dtype=torch.uint8, device="cuda")
@@ -191,19 +205,27 @@ def build_copies(cfg, n_copies):
     return copies, stride, act
 
 
-def algorithmic_units(cfg, counts):
-    """Packed-expert bytes and FLOPs one call must touch, from the routed counts."""
+def algorithmic_units(cfg, counts, fmt="int8"):
+    """Packed-expert bytes and FLOPs one call must touch, from the routed counts.
+    INT8: gate and up (2RC) plus the shared scales (2R bytes) for gate/up, RC
+    for down; INT4: the 544-byte tiles (nibbles and their fp16 scales) of
+    gate and up, then of down."""
     active = [g for g in range(cfg.G) if counts[g] > 0]
     pairs = int(sum(counts))
-    gu_bytes = len(active) * (2 * cfg.R * cfg.C + 2 * cfg.R)
-    dn_bytes = len(active) * (cfg.C * cfg.R)
+    if fmt == "int4":
+        tiles = (cfg.R // 16) * (cfg.C // 64)
+        gu_bytes = len(active) * 2 * tiles * 544
+        dn_bytes = len(active) * tiles * 544
+    else:
+        gu_bytes = len(active) * (2 * cfg.R * cfg.C + 2 * cfg.R)
+        dn_bytes = len(active) * (cfg.C * cfg.R)
     gu_flops = pairs * 4.0 * cfg.C * cfg.R
     dn_flops = pairs * 2.0 * cfg.C * cfg.R
     return dict(active=len(active), pairs=pairs, gu_bytes=gu_bytes, dn_bytes=dn_bytes,
                 gu_flops=gu_flops, dn_flops=dn_flops)
 
 
-def cpu_baseline(cfg, copy0, budget_s):
+def cpu_baseline(cfg, copy0, budget_s, fmt="int8"):
     """The oracle, as it stands, on a bounded sample of the same workload."""
     import numpy as np
     import oracle
@@ -218,6 +240,7 @@ def cpu_baseline(cfg, copy0, budget_s):
     b = None if copy0["bias"] is None else copy0["bias"].cpu().numpy().astype(np.float64)
     logits = oracle.router_logits(x, wr, b)
     idx = oracle.topk_select(logits, cfg.k)
+    pack = oracle.pack_expert_int4 if fmt == "int4" else oracle.pack_expert
     # pack the experts the sample needs (offline step, timed separately)
     t0 = time.perf_counter()
     blobs = {}
@@ -227,11 +250,11 @@ def cpu_baseline(cfg, copy0, budget_s):
         need = [int(e) for e in idx[t] if int(e) not in blobs]
         for e in need:
             wg, wu, wd = (w.cpu().numpy() for w in expert_weights(cfg, 0, e, "cuda"))
-            blobs[e] = oracle.pack_expert(wg, wu, wd)
+            blobs[e] = pack(wg, wu, wd)
         tokens.append(t)
         if time.perf_counter() > deadline or len(tokens) >= 64:
             break
-    shared = [oracle.pack_expert(*(w.cpu().numpy() for w in expert_weights(cfg, 0, cfg.E + s, "cuda")))
+    shared = [pack(*(w.cpu().numpy() for w in expert_weights(cfg, 0, cfg.E + s, "cuda")))
               for s in range(cfg.S)]
     pack_s = time.perf_counter() - t0
 
@@ -246,7 +269,8 @@ def cpu_baseline(cfg, copy0, budget_s):
     t1 = time.perf_counter()
     reps = 0
     while True:
-        oracle.moe_forward(x, wr, b, Blobs(), cfg.k, cfg.C, cfg.R, shared_blobs=shared, tokens=tokens)
+        oracle.moe_forward(x, wr, b, Blobs(), cfg.k, cfg.C, cfg.R, shared_blobs=shared, tokens=tokens,
+                           fmt=fmt)
         reps += 1
         if time.perf_counter() - t1 >= budget_s or reps >= 1000:
             break
@@ -256,7 +280,8 @@ def cpu_baseline(cfg, copy0, budget_s):
         "unit": "tokens/s",
         "cores": int(blas_threads),
         "kind": "oracle",
-        "sample": (f"numpy fp64 oracle forward (router, top-k, expert FFN one expert at a time, combine) "
+        "sample": (f"numpy fp64 oracle forward ({fmt} experts; router, top-k, expert FFN one expert at a "
+                   f"time, combine) "
                    f"on the first {len(tokens)} token(s) of layer copy 0 of the same workload; "
                    f"{len(blobs) + len(shared)} experts packed beforehand in {pack_s:.1f} s (not timed); "
                    f"{reps} forward pass(es) over the sample took {fwd_s:.2f} s; "
@@ -568,15 +593,20 @@ def main():
 
     mira.load()
     cfg = CONFIGS[args.workload]
+    fmt = args.format
+    if fmt == "int4" and (cfg.layers > 1 or cfg.T > mira.MIRA_DECODE_MAX_TOKENS):
+        print(json.dumps({"error": "the INT4 variant runs on the decode kernels: use a single-layer "
+                                   "decode workload (mixtral_decode, tiny)", "workload": cfg.name}))
+        return 2
     if cfg.layers > 1:
         return run_stack(args, cfg)
     # bytes of packed experts one call can touch: at most min(G, T*k + S) experts
-    touched = min(cfg.G, cfg.T * cfg.k + cfg.S) * mira.mira_packed_expert_bytes(cfg.C, cfg.R)
+    touched = min(cfg.G, cfg.T * cfg.k + cfg.S) * expert_stride(cfg, fmt)
     n_copies = max(2, min(8, math.ceil(COLD_BYTES / max(1, touched)) + 1))
     if cfg.name == "tiny":
         n_copies = 1
-    copies, stride, act = build_copies(cfg, n_copies)
-    shape = mira.MoEShape(cfg.C, cfg.R, cfg.E, cfg.k, cfg.S, act, 0)
+    copies, stride, act = build_copies(cfg, n_copies, fmt)
+    shape = mira.MoEShape(cfg.C, cfg.R, cfg.E, cfg.k, cfg.S, act, format_flag(fmt))
     T = cfg.T
     ws = torch.empty(mira.mira_workspace_bytes(shape, T), dtype=torch.uint8, device="cuda")
     out = torch.empty((T, cfg.C), dtype=torch.float32, device="cuda")
@@ -610,7 +640,7 @@ def main():
     for i in range(len(argsets)):
         step(i)
         torch.cuda.synchronize()
-        units.append(algorithmic_units(cfg, counts.cpu().tolist()))
+        units.append(algorithmic_units(cfg, counts.cpu().tolist(), fmt))
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
@@ -648,7 +678,8 @@ def main():
                 achieved = avg["gu_bytes"] / dur / 1e9
                 roof = {"bound": "hbm", "kernel": name, "achieved": round(achieved, 1),
                         "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                        "traffic": traffic_bytes(name, cfg.name), "avg_us": round(dur * 1e6, 2),
+                        "traffic": traffic_bytes(name, cfg.name if fmt == "int8" else f"{cfg.name}_int4"),
+                        "avg_us": round(dur * 1e6, 2),
                         "algorithmic_bytes_per_launch": int(avg["gu_bytes"])}
         else:
             name = "prefill_gateup"
@@ -676,7 +707,7 @@ def main():
         "vs_baseline": None,
         "dtype": "i8" if decode else "bf16",
         "data": "synthetic",
-        "config": {"workload": cfg.name, "tokens": T, "hidden": cfg.C, "experts": cfg.E,
+        "config": {"workload": cfg.name, "format": fmt, "tokens": T, "hidden": cfg.C, "experts": cfg.E,
                    "top_k": cfg.k, "ffn": cfg.R, "shared_experts": cfg.S,
                    "activations": cfg.act, "layer_copies": len(copies),
                    "experts_touched_per_step": round(avg["active"], 2)},
@@ -686,7 +717,7 @@ def main():
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(cfg, copies[0], args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(cfg, copies[0], args.cpu_seconds, fmt)
     print(json.dumps(line), flush=True)
     return 0
 

@@ -68,6 +68,13 @@ typedef enum mira_dtype {
 /* Force the grouped-GEMM (prefill) expert kernels for any n_tokens. */
 #define MIRA_FLAG_FORCE_PREFILL 0x4u
 
+/* Experts are in the INT4 variant format below (4-bit values, one fp16 scale
+ * per row and group of 64 columns) instead of the paper's INT8 format.  INT4
+ * layers run on the decode kernels only: n_tokens must satisfy the decode
+ * limits and MIRA_FLAG_FORCE_PREFILL is rejected (MIRA_ERR_UNSUPPORTED).
+ * mira_pack_experts reads this bit to choose the format it writes. */
+#define MIRA_FLAG_INT4 0x8u
+
 /* Without a FORCE flag, calls with n_tokens <= this use the decode kernels. */
 #define MIRA_DECODE_MAX_TOKENS 16
 
@@ -99,6 +106,24 @@ typedef enum mira_dtype {
  * Returns 0 if hidden or ffn is not positive or the size overflows. */
 size_t mira_packed_expert_bytes(int32_t hidden, int32_t ffn);
 
+/* ---- INT4 variant of the packed expert (MIRA_FLAG_INT4) -----------------
+ * The 4-bit, group-64, fp16-scale format (the paper keeps INT8, section IV-B,
+ * and lists INT4 as a quality point, Table I).  Per matrix [rows][K]
+ * (gate [R][C], up [R][C], down [C][R], each with its own scales) and per row
+ * and group of 64 consecutive columns:
+ *   alpha = max |w| over the group (exact),
+ *   s     = fp16 of fl32(max(alpha, eps) / 7), round to nearest even; 2^-24
+ *           if that rounds to zero, 65504 if it overflows,
+ *   q     = clamp(rint_even(fl32(w / s)), -7, 7),  the weight is s * q.
+ * Each matrix is stored as 16 x 64 tiles (tile-rows in order, column blocks
+ * in order) of 544 bytes: 512 bytes of nibbles, then the 16 little-endian
+ * fp16 scales of the tile's rows for its column block.  Inside a tile, the
+ * 8-byte run g*16 + i holds row i, columns 16g .. 16g+15: byte b (0..7)
+ * carries column 16g + 8*(b/4) + b%4 in its high nibble and that column + 4
+ * in its low nibble, each as the two's complement of q.  gate, up and down
+ * follow each other, zero-padded to a multiple of 256 bytes. */
+size_t mira_packed_expert_bytes_int4(int32_t hidden, int32_t ffn);
+
 /* Shape of one MoE layer. */
 typedef struct mira_shape {
   int32_t hidden;    /* C: model hidden size; multiple of 64 */
@@ -120,7 +145,10 @@ typedef struct mira_shape {
  *   eps: the paper's small constant (positive, finite), e.g. 1e-8.
  *   on_device = 0: host pointers; runs on host threads and returns when done
  *     (stream ignored).  on_device = 1: device pointers; enqueued on stream.
- * Both paths produce identical bytes.  Only s->hidden and s->ffn are read. */
+ * Both paths produce identical bytes.  Only s->hidden, s->ffn and the
+ * MIRA_FLAG_INT4 bit of s->flags are read; with that bit the experts are
+ * written in the INT4 variant and packed_stride must be a multiple of 256 and
+ * >= mira_packed_expert_bytes_int4(C, R). */
 int mira_pack_experts(const mira_shape* s, int32_t n_experts, int32_t w_dtype,
                       const void* w_gate, const void* w_up, const void* w_down,
                       float eps, void* packed, uint64_t packed_stride,
@@ -137,7 +165,8 @@ typedef struct mira_moe_args {
                                 experts first, then shared), or -1 when the
                                 expert is not resident */
   const void* slot_pool;     /* n_slots * slot_stride bytes of packed experts */
-  uint64_t slot_stride;      /* multiple of 256, >= mira_packed_expert_bytes(C, R) */
+  uint64_t slot_stride;      /* multiple of 256, >= mira_packed_expert_bytes(C, R)
+                                (mira_packed_expert_bytes_int4 with MIRA_FLAG_INT4) */
   float* out;                /* [T][C] fp32: sum_j w[t,j] * expert_{idx[t,j]}(x_t)
                                 plus the shared experts' outputs */
   int32_t* topk_idx;         /* optional [T][k]: selected experts, best first */

@@ -38,13 +38,16 @@ notes of the repository):
   result of zero becomes the smallest positive fp16 2^-24, an overflow the
   largest finite 65504), and q = clamp(round_half_even(fl32(w / s)), -7, 7)
   against that stored s.  gate, up and down each carry their own scales.
-* INT4 byte layout: each matrix [rows][K] is cut into 16 x 64 tiles stored
-  like the INT8 tiles (tile-rows in order, column blocks in order); a tile is
-  544 bytes: 512 bytes of nibbles, then the 16 fp16 scales of its rows for
-  its column block.  Run g*16 + i (8 bytes) holds row i, columns
-  16g .. 16g+15: byte b (0..7) carries column 16g + 8*(b//4) + (b%4) in its
-  high nibble and column 16g + 8*(b//4) + 4 + (b%4) in its low nibble, each
-  nibble the two's complement of q.
+* INT4 byte layout (rows and K multiples of 16 and 128): each matrix
+  [rows][K] is a nibble region followed by a scale region.  Nibbles: tiles of
+  16 rows x 128 columns (two groups), 1024 bytes each, tile-rows in order and
+  column pairs in order; inside a tile the 16-byte run g*16 + i holds row i,
+  columns 16g .. 16g+15 of the first group in its bytes 0..7 and of the
+  second group in bytes 8..15; in each 8-byte half, byte b carries column
+  16g + 8*(b//4) + (b%4) in its high nibble and that column + 4 in its low
+  nibble, each nibble the two's complement of q.  Scales: fp16 (little
+  endian), ordered by tile-row, then group, then the 16 rows of the tile
+  (32 bytes per tile-row and group).
 * Permutation: (token, slot) pairs p = t*k + j are grouped by expert with a
   stable counting sort; shared-expert pairs follow the routed ones, in token
   order.
@@ -78,7 +81,7 @@ __all__ = [
     "pack_expert",
     "unpack_expert",
     "dequantize_expert",
-    "INT4_TILE_BYTES",
+    "int4_matrix_bytes",
     "packed_expert_bytes_int4",
     "int4_tile_order",
     "int4_untile_order",
@@ -241,13 +244,17 @@ def dequantize_expert(blob, C: int, R: int):
 # INT4 variant: group-64 scales in fp16 (Table I's INT4 point)
 # ----------------------------------------------------------------------------
 
-INT4_TILE_BYTES = 544   # 16 x 64 nibbles (512 bytes) + 16 fp16 row scales
 INT4_QMAX = 7
 
 
+def int4_matrix_bytes(rows: int, K: int) -> int:
+    """Nibbles (rows*K/2) plus fp16 scales (rows*K/64 of them) of one INT4 matrix."""
+    return rows * K // 2 + rows * (K // 64) * 2
+
+
 def packed_expert_bytes_int4(C: int, R: int) -> int:
-    """Bytes of one INT4 expert: 3 * (R/16) * (C/64) tiles of 544 bytes, padded to 256."""
-    n = 3 * (R // 16) * (C // 64) * INT4_TILE_BYTES
+    """Bytes of one INT4 expert: gate, up and down matrices, padded to 256."""
+    n = 2 * int4_matrix_bytes(R, C) + int4_matrix_bytes(C, R)
     return (n + BLOB_ALIGN - 1) // BLOB_ALIGN * BLOB_ALIGN
 
 
@@ -276,30 +283,32 @@ def int4_tile_order(q, s16):
     """Bytes of one INT4 matrix q [rows][K] with its scales s16 [rows][K/64]."""
     q = np.asarray(q)
     rows, K = q.shape
-    if rows % 16 or K % 64:
-        raise ValueError("tiled layout needs rows % 16 == 0 and K % 64 == 0")
+    if rows % 16 or K % 128:
+        raise ValueError("the INT4 layout needs rows % 16 == 0 and K % 128 == 0")
     nib = (q.astype(np.int16) & 0xF).astype(np.uint8)
-    # column inside a 64-block = 16g + 8h + 4p + j; p = 0 high nibble, 1 low nibble
-    t = nib.reshape(rows // 16, 16, K // 64, 4, 2, 2, 4)          # [tr][i][blk][g][h][p][j]
-    byte = (t[:, :, :, :, :, 0, :] << 4) | t[:, :, :, :, :, 1, :]  # [tr][i][blk][g][h][j]
-    byte = byte.transpose(0, 2, 3, 1, 4, 5).reshape(rows // 16, K // 64, 512)
+    # column inside a 128-column tile = 64e + 16g + 8h + 4p + j: e the group of
+    # the pair, p = 0 high nibble, 1 low nibble
+    t = nib.reshape(rows // 16, 16, K // 128, 2, 4, 2, 2, 4)          # [tr][i][pair][e][g][h][p][j]
+    byte = (t[..., 0, :] << 4) | t[..., 1, :]                          # [tr][i][pair][e][g][h][j]
+    byte = byte.transpose(0, 2, 4, 1, 3, 5, 6).reshape(-1)             # [tr][pair][g][i][e][h][j]
     sc = np.asarray(s16, dtype="<f2").reshape(rows // 16, 16, K // 64).transpose(0, 2, 1)
-    sc = np.ascontiguousarray(sc).view(np.uint8).reshape(rows // 16, K // 64, 32)
-    return np.concatenate([byte.astype(np.uint8), sc], axis=2).reshape(-1)
+    sc = np.ascontiguousarray(sc).view(np.uint8).reshape(-1)           # [tr][group][i]
+    return np.concatenate([byte.astype(np.uint8), sc])
 
 
 def int4_untile_order(flat, rows, K):
     """Inverse of int4_tile_order: (q [rows][K] int8, s16 [rows][K/64])."""
-    t = np.asarray(flat, dtype=np.uint8).reshape(rows // 16, K // 64, INT4_TILE_BYTES)
-    b = t[:, :, :512].reshape(rows // 16, K // 64, 4, 16, 2, 4)   # [tr][blk][g][i][h][j]
+    flat = np.asarray(flat, dtype=np.uint8)
+    nb = rows * K // 2
+    b = flat[:nb].reshape(rows // 16, K // 128, 4, 16, 2, 2, 4)      # [tr][pair][g][i][e][h][j]
     hi = (b >> 4).astype(np.int16)
     lo = (b & 0xF).astype(np.int16)
     hi = np.where(hi >= 8, hi - 16, hi)
     lo = np.where(lo >= 8, lo - 16, lo)
-    q = np.stack([hi, lo], axis=5)                                 # [tr][blk][g][i][h][p][j]
-    q = q.transpose(0, 3, 1, 2, 4, 5, 6).reshape(rows, K).astype(np.int8)
-    sc = np.ascontiguousarray(t[:, :, 512:]).view("<f2").reshape(rows // 16, K // 64, 16)
-    s16 = sc.transpose(0, 2, 1).reshape(rows, K // 64).astype(np.float16)
+    q = np.stack([hi, lo], axis=6)                                     # [tr][pair][g][i][e][h][p][j]
+    q = q.transpose(0, 3, 1, 4, 2, 5, 6, 7).reshape(rows, K).astype(np.int8)
+    sc = np.ascontiguousarray(flat[nb:nb + rows * (K // 64) * 2]).view("<f2")
+    s16 = sc.reshape(rows // 16, K // 64, 16).transpose(0, 2, 1).reshape(rows, K // 64).astype(np.float16)
     return q, s16
 
 
@@ -311,8 +320,8 @@ def pack_expert_int4(w_gate, w_up, w_down, eps=1e-8):
     R, C = w_gate.shape
     if w_up.shape != (R, C) or w_down.shape != (C, R):
         raise ValueError("expected gate/up [R][C] and down [C][R]")
-    if R % 64 or C % 64:
-        raise ValueError("C and R must be multiples of 64")
+    if R % 128 or C % 128:
+        raise ValueError("C and R must be multiples of 128 in the INT4 layout")
     if not (np.all(np.isfinite(w_gate)) and np.all(np.isfinite(w_up)) and np.all(np.isfinite(w_down))):
         raise ValueError("non-finite weights are out of contract")
     blob = np.zeros(packed_expert_bytes_int4(C, R), dtype=np.uint8)
@@ -328,7 +337,7 @@ def pack_expert_int4(w_gate, w_up, w_down, eps=1e-8):
 def unpack_expert_int4(blob, C: int, R: int):
     """((q_gate, s_gate), (q_up, s_up), (q_down, s_down)) of an INT4 blob."""
     blob = np.asarray(blob, dtype=np.uint8)
-    n = (R // 16) * (C // 64) * INT4_TILE_BYTES
+    n = int4_matrix_bytes(R, C)
     if blob.size < 3 * n:
         raise ValueError("blob too small for the given shape")
     return (int4_untile_order(blob[0:n], R, C), int4_untile_order(blob[n:2 * n], R, C),

@@ -14,6 +14,7 @@ from ._binding import (  # noqa: F401
     MIRA_F32,
     MIRA_FLAG_FORCE_DECODE,
     MIRA_FLAG_FORCE_PREFILL,
+    MIRA_FLAG_INT4,
     MIRA_FLAG_SOFTMAX_ALL,
     MIRA_MAX_EXPERTS,
     MIRA_MAX_TOPK,
@@ -31,6 +32,7 @@ from ._binding import (  # noqa: F401
     mira_moe_route,
     mira_pack_experts,
     mira_packed_expert_bytes,
+    mira_packed_expert_bytes_int4,
     mira_mixture_workspace_bytes,
     mira_predict,
     mira_predict_mixture,
@@ -46,6 +48,7 @@ from ._binding import (  # noqa: F401
 
 EXPORTED_SYMBOLS = (
     "mira_packed_expert_bytes",
+    "mira_packed_expert_bytes_int4",
     "mira_workspace_bytes",
     "mira_pack_experts",
     "mira_moe_forward",

@@ -15,6 +15,7 @@ MIRA_BF16 = 1
 MIRA_FLAG_SOFTMAX_ALL = 0x1
 MIRA_FLAG_FORCE_DECODE = 0x2
 MIRA_FLAG_FORCE_PREFILL = 0x4
+MIRA_FLAG_INT4 = 0x8
 MIRA_DECODE_MAX_TOKENS = 16
 MIRA_MAX_EXPERTS = 256
 MIRA_MAX_TOPK = 16
@@ -206,6 +207,7 @@ def load():
                                       ctypes.c_uint64, ctypes.c_float, ctypes.c_size_t)
         sig = {
             "mira_packed_expert_bytes": (sz, [i32, i32]),
+            "mira_packed_expert_bytes_int4": (sz, [i32, i32]),
             "mira_workspace_bytes": (sz, [ctypes.POINTER(_Shape), i32]),
             "mira_pack_experts": (ctypes.c_int, [ctypes.POINTER(_Shape), i32, i32, vp, vp, vp, f32, vp,
                                                  u64, i32, vp]),
@@ -254,6 +256,10 @@ def mira_version() -> str:
 
 def mira_packed_expert_bytes(hidden: int, ffn: int) -> int:
     return int(load().mira_packed_expert_bytes(hidden, ffn))
+
+
+def mira_packed_expert_bytes_int4(hidden: int, ffn: int) -> int:
+    return int(load().mira_packed_expert_bytes_int4(hidden, ffn))
 
 
 def mira_workspace_bytes(shape: MoEShape, max_tokens: int) -> int:

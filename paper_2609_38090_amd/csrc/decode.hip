@@ -18,12 +18,19 @@ namespace mira {
 // the digits of x come from the workspace (xdig[(t*3 + d)*C + c], written by
 // the decode preparation kernel).
 // ---------------------------------------------------------------------------
-template <int NG>
-__global__ __launch_bounds__(256) void decode_gateup_kernel(int C, int R, ExpertPool ep,
-                                                            const DecodeWork* __restrict__ work,
-                                                            const int8_t* __restrict__ xdig,
-                                                            int8_t* __restrict__ hdig,
-                                                            int32_t* __restrict__ hexp) {
+// With XL (INT4, one token group, C <= kXlMaxC) the workgroup first copies
+// the digit rows of its tokens into LDS (row stride C + 16 bytes, so the 16
+// rows a read phase touches fall in distinct banks) and the loop reads them
+// from there.
+constexpr int kXlMaxC = 4096;
+constexpr int kXlUnroll = 16;  // k-steps per weight batch
+
+template <int NG, bool I4, bool XL>
+__device__ __forceinline__ void decode_gateup_body(int C, int R, const ExpertPool& ep,
+                                                   const DecodeWork* __restrict__ work,
+                                                   const int8_t* __restrict__ xdig,
+                                                   int8_t* __restrict__ hdig,
+                                                   int32_t* __restrict__ hexp) {
   __shared__ float bmax[4][NG * kTokPerGroup];
   const int nrb = R / kBlk;
   const int a = blockIdx.x / nrb, rb = blockIdx.x - a * nrb;
@@ -50,8 +57,55 @@ __global__ __launch_bounds__(256) void decode_gateup_kernel(int C, int R, Expert
     xev[cg] = bv[cg] ? wk.xe[i] : 0;
     bp[cg] = xdig + ((size_t)tok * kDigits + d) * C + kg * 16;
   }
-  gateup_block<NG>(C, R, rb, ep.pool + (size_t)slot * ep.stride, wk.off, bv, xev,
-                   [&](int cg, int ks) { return ld16(bp[cg] + ks * 64); }, hdig, hexp, bmax);
+  if constexpr (XL) {
+    static_assert(NG == 1, "one token group in LDS");
+    __shared__ __attribute__((aligned(16))) int8_t xl[16 * (kXlMaxC + 16)];
+    const int ld = C + 16;
+    const int chunks = C / 16;
+    for (int i = threadIdx.x; i < NG * 16 * chunks; i += 256) {
+      const int row = i / chunks, c16 = i - row * chunks;
+      const int cg = row >> 4, col = row & 15;
+      const int mm = col / 3, dd = col - 3 * mm, ti = cg * kTokPerGroup + mm;
+      v4i v = zero16();
+      if (col < 3 * kTokPerGroup && ti < n)
+        v = ld16(xdig + ((size_t)wk.tok[ti] * kDigits + dd) * C + c16 * 16);
+      *(v4i*)(xl + (size_t)row * ld + c16 * 16) = v;
+    }
+    __syncthreads();
+    const int8_t* xr[NG];
+#pragma unroll
+    for (int cg = 0; cg < NG; ++cg) xr[cg] = xl + (size_t)(cg * 16 + r16) * ld + kg * 16;
+    const auto load_x = [&](int cg, int ks) { return *(const v4i*)(xr[cg] + ks * 64); };
+    gateup_block_i4<NG, kXlUnroll, true>(C, R, rb, (const uint8_t*)ep.pool + (size_t)slot * ep.stride,
+                                         wk.off, bv, xev, load_x, hdig, hexp, bmax);
+    return;
+  }
+  const auto load_b = [&](int cg, int ks) { return ld16(bp[cg] + ks * 64); };
+  if constexpr (I4)
+    gateup_block_i4<NG, dec_unroll(NG), false>(C, R, rb,
+                                               (const uint8_t*)ep.pool + (size_t)slot * ep.stride,
+                                               wk.off, bv, xev, load_b, hdig, hexp, bmax);
+  else
+    gateup_block<NG>(C, R, rb, ep.pool + (size_t)slot * ep.stride, wk.off, bv, xev, load_b, hdig,
+                     hexp, bmax);
+}
+
+template <int NG, bool I4>
+__global__ __launch_bounds__(256) void decode_gateup_kernel(int C, int R, ExpertPool ep,
+                                                            const DecodeWork* __restrict__ work,
+                                                            const int8_t* __restrict__ xdig,
+                                                            int8_t* __restrict__ hdig,
+                                                            int32_t* __restrict__ hexp) {
+  decode_gateup_body<NG, I4, false>(C, R, ep, work, xdig, hdig, hexp);
+}
+
+// The LDS variant keeps two workgroups per CU (the 64 KB of digits each).
+__global__ __launch_bounds__(256, 2) void decode_gateup_xl_kernel(int C, int R, ExpertPool ep,
+                                                                 const DecodeWork* __restrict__ work,
+                                                                 const int8_t* __restrict__ xdig,
+                                                                 int8_t* __restrict__ hdig,
+                                                                 int32_t* __restrict__ hexp) {
+  decode_gateup_body<1, true, true>(C, R, ep, work, xdig, hdig, hexp);
 }
 
 // ---------------------------------------------------------------------------
@@ -61,7 +115,7 @@ __global__ __launch_bounds__(256) void decode_gateup_kernel(int C, int R, Expert
 // (token, expert) pair and summed per token in a fixed order (expert list
 // order inside a wave, then wave order), so the result is deterministic.
 // ---------------------------------------------------------------------------
-template <int NG, int KS>
+template <int NG, int KS, bool I4>
 __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
     int C, int R, int T, int max_active, ExpertPool ep, const DecodeWork* __restrict__ work,
     const int8_t* __restrict__ hdig, const int32_t* __restrict__ hexp, float* __restrict__ out) {
@@ -73,7 +127,8 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
   const int r16 = lane & 15, kg = lane >> 4;
   const int m = r16 / 3, d = r16 - 3 * m;
   const int nks = R / 64;
-  const int spw = (nks + KS - 1) / KS;
+  // k-steps per wave; even for INT4, whose loads cover two k-steps
+  const int spw = I4 ? (((nks + KS - 1) / KS + 1) & ~1) : (nks + KS - 1) / KS;
   const int ks_beg = wave * spw, ks_end = min(nks, ks_beg + spw);
 
   for (int a = 0; a < max_active; ++a) {
@@ -83,8 +138,15 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
     const int slot = ep.slot_table[g];
     if (slot < 0 || slot >= ep.n_slots) continue;
     const int off = wk.off, n = wk.n;
-    const int8_t* dp = ep.pool + (size_t)slot * ep.stride + (size_t)2 * R * C +
-                       (size_t)blockIdx.x * nks * 1024 + lane * 16;  // tile row c0/16
+    // tile row c0/16 of the down matrix: INT8 tiles of 1 KB (lane l at 16*l),
+    // or INT4 nibble tiles of two groups (lane l at 16*l) and the tile-row's
+    // 32-byte scale blocks (lane l at 8*l of a 16-group run)
+    const int8_t* base = ep.pool + (size_t)slot * ep.stride;
+    const int8_t* dp = I4 ? base + 2 * i4_matrix_bytes(R, C) + (size_t)blockIdx.x * (nks / 2) * kI4PairTile +
+                                lane * 16
+                          : base + (size_t)2 * R * C + (size_t)blockIdx.x * nks * 1024 + lane * 16;
+    const int8_t* sp = base + 2 * i4_matrix_bytes(R, C) + i4_nib_bytes(C, R) +
+                       (size_t)blockIdx.x * nks * 32 + lane * 8;
     const int8_t* bp[NG];
     const int32_t* hx[NG];
     bool bv[NG];
@@ -103,16 +165,27 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
       for (int i = 0; i < 4; ++i) facc[cg][i] = 0.f;
 
     constexpr int kDecUnroll = dec_unroll(NG);
+    static_assert(kDecUnroll % 2 == 0 && kDecUnroll <= 16, "INT4 batches cover whole tiles");
     struct Batch {
-      v4i a[kDecUnroll], b[kDecUnroll][NG];
+      v4i a[I4 ? kDecUnroll / 2 : kDecUnroll], b[kDecUnroll][NG];
+      uint2 s4;  // INT4: lane l holds group ks0 + l/4, rows 4*(l%4) .. +3
       int he[kDecUnroll][NG];
-    } b0, b1;
+    };
     auto issue = [&](Batch& bt, int ks0) {
+      if constexpr (I4) {
+#pragma unroll
+        for (int p = 0; p < kDecUnroll / 2; ++p) {
+          const bool in = ks0 + 2 * p < ks_end;
+          bt.a[p] = in ? ld16_stream(dp + (size_t)(ks0 / 2 + p) * kI4PairTile) : zero16();
+        }
+        const bool sin = (lane >> 2) < kDecUnroll && ks0 + (lane >> 2) < ks_end;
+        bt.s4 = sin ? ld8_stream(sp + (size_t)ks0 * 32) : uint2{0, 0};
+      }
 #pragma unroll
       for (int u = 0; u < kDecUnroll; ++u) {
         const int ks = ks0 + u;
         const bool in = ks < ks_end;
-        bt.a[u] = in ? ld16_stream(dp + ks * 1024) : zero16();
+        if constexpr (!I4) bt.a[u] = in ? ld16_stream(dp + ks * 1024) : zero16();
 #pragma unroll
         for (int cg = 0; cg < NG; ++cg) {
           bt.b[u][cg] = (in && bv[cg]) ? ld16(bp[cg] + ks * 64) : zero16();
@@ -122,21 +195,33 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
     };
     auto consume = [&](const Batch& bt) {
 #pragma unroll
-      for (int u = 0; u < kDecUnroll; ++u)
+      for (int u = 0; u < kDecUnroll; ++u) {
+        v4i a;
+        float s4[4] = {1.f, 1.f, 1.f, 1.f};
+        if constexpr (I4) {
+          const v4i q2 = bt.a[u / 2];
+          a = (u & 1) ? i4_operand(uint2{(uint32_t)q2[2], (uint32_t)q2[3]})
+                      : i4_operand(uint2{(uint32_t)q2[0], (uint32_t)q2[1]});
+          i4_scales(uint2{(uint32_t)__shfl((int)bt.s4.x, 4 * u + kg, 64),
+                          (uint32_t)__shfl((int)bt.s4.y, 4 * u + kg, 64)}, s4);
+        } else {
+          a = bt.a[u];
+        }
 #pragma unroll
         for (int cg = 0; cg < NG; ++cg) {
-          const v4i sres = mfma_i8(bt.a[u], bt.b[u][cg], zero16());
-          const float sc = bv[cg] ? ldexpf(1.f, 8 * d - bt.he[u][cg]) : 0.f;
+          const v4i sres = mfma_i8(a, bt.b[u][cg], zero16());
+          // digit weight and H' exponent; INT4 adds the row scales and 1/16
+          const float sc = bv[cg] ? ldexpf(1.f, 8 * d - bt.he[u][cg] - (I4 ? 4 : 0)) : 0.f;
 #pragma unroll
-          for (int i = 0; i < 4; ++i) facc[cg][i] = fmaf((float)sres[i], sc, facc[cg][i]);
+          for (int i = 0; i < 4; ++i) facc[cg][i] = fmaf((float)sres[i], sc * s4[i], facc[cg][i]);
         }
+      }
     };
-    issue(b0, ks_beg);
-    for (int ks = ks_beg; ks < ks_end; ks += 2 * kDecUnroll) {
-      issue(b1, ks + kDecUnroll);
-      consume(b0);
-      issue(b0, ks + 2 * kDecUnroll);
-      consume(b1);
+    // one batch per iteration (see the gate/up body)
+    for (int ks = ks_beg; ks < ks_end; ks += kDecUnroll) {
+      Batch bt;
+      issue(bt, ks);
+      consume(bt);
     }
 #pragma unroll
     for (int cg = 0; cg < NG; ++cg) {
@@ -164,47 +249,52 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
 
 constexpr int kDownKS = 8;
 
-template <int NG>
+template <int NG, bool I4>
 static void launch_decode_down_ng(const Layout& L, const WsPtr& w, const ExpertPool& ep,
                                   float* out, hipStream_t st) {
-  launch_timed("decode_down", (decode_down_kernel<NG, kDownKS>), dim3(L.C / 16), dim3(64 * kDownKS),
-               0, st, L.C, L.R, L.T, decode_max_active(L), ep, w.dwork, w.hdig, w.hexp, out);
+  launch_timed("decode_down", (decode_down_kernel<NG, kDownKS, I4>), dim3(L.C / 16),
+               dim3(64 * kDownKS), 0, st, L.C, L.R, L.T, decode_max_active(L), ep, w.dwork, w.hdig,
+               w.hexp, out);
 }
 
-template <int NG>
+template <int NG, bool I4>
 static void launch_decode_ffn(const Layout& L, const WsPtr& w, const ExpertPool& ep, float* out,
                               hipStream_t st) {
   const int nrb = L.R / kBlk;
   const int max_active = decode_max_active(L);
-  launch_timed("decode_gateup", decode_gateup_kernel<NG>, dim3(max_active * nrb), dim3(256), 0, st,
-               L.C, L.R, ep, w.dwork, w.xdig, w.hdig, w.hexp);
-  launch_decode_down_ng<NG>(L, w, ep, out, st);
-}
-
-hipError_t launch_decode_down(const Layout& L, const WsPtr& w, const ExpertPool& ep, float* out,
-                              hipStream_t st) {
-  if (L.T == 0) return hipSuccess;
-  switch ((L.T + kTokPerGroup - 1) / kTokPerGroup) {
-    case 1: launch_decode_down_ng<1>(L, w, ep, out, st); break;
-    case 2: launch_decode_down_ng<2>(L, w, ep, out, st); break;
-    case 3: launch_decode_down_ng<3>(L, w, ep, out, st); break;
-    default: launch_decode_down_ng<4>(L, w, ep, out, st); break;
+  if constexpr (I4 && NG == 1) {
+    if (L.C <= kXlMaxC) {
+      launch_timed("decode_gateup", decode_gateup_xl_kernel, dim3(max_active * nrb), dim3(256), 0, st,
+                   L.C, L.R, ep, w.dwork, w.xdig, w.hdig, w.hexp);
+      launch_decode_down_ng<NG, I4>(L, w, ep, out, st);
+      return;
+    }
   }
-  return hipGetLastError();
+  launch_timed("decode_gateup", (decode_gateup_kernel<NG, I4>), dim3(max_active * nrb),
+               dim3(256), 0, st, L.C, L.R, ep, w.dwork, w.xdig, w.hdig, w.hexp);
+  launch_decode_down_ng<NG, I4>(L, w, ep, out, st);
 }
 
 hipError_t launch_decode(const mira_shape& s, const Layout& L, const WsPtr& w, const void* x,
                          const ExpertPool& ep, float* out, hipStream_t st) {
-  (void)s;
   (void)x;  // x enters through the fixed-point digits written by decode_prep_kernel
   const int T = L.T;
   if (T == 0) return hipSuccess;
   const int ng = (T + kTokPerGroup - 1) / kTokPerGroup;  // every group holds <= T tokens
-  switch (ng) {
-    case 1: launch_decode_ffn<1>(L, w, ep, out, st); break;
-    case 2: launch_decode_ffn<2>(L, w, ep, out, st); break;
-    case 3: launch_decode_ffn<3>(L, w, ep, out, st); break;
-    default: launch_decode_ffn<4>(L, w, ep, out, st); break;
+  if (s.flags & MIRA_FLAG_INT4) {
+    switch (ng) {
+      case 1: launch_decode_ffn<1, true>(L, w, ep, out, st); break;
+      case 2: launch_decode_ffn<2, true>(L, w, ep, out, st); break;
+      case 3: launch_decode_ffn<3, true>(L, w, ep, out, st); break;
+      default: launch_decode_ffn<4, true>(L, w, ep, out, st); break;
+    }
+  } else {
+    switch (ng) {
+      case 1: launch_decode_ffn<1, false>(L, w, ep, out, st); break;
+      case 2: launch_decode_ffn<2, false>(L, w, ep, out, st); break;
+      case 3: launch_decode_ffn<3, false>(L, w, ep, out, st); break;
+      default: launch_decode_ffn<4, false>(L, w, ep, out, st); break;
+    }
   }
   return hipGetLastError();
 }

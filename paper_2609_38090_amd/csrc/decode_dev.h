@@ -13,6 +13,7 @@
 #pragma once
 
 #include "device_util.h"
+#include "int4_format.h"
 #include "mira_internal.h"
 
 namespace mira {
@@ -27,7 +28,47 @@ __device__ __forceinline__ float combine_digits_i(int s0) {
 }
 
 // k-steps per load batch; fewer when many token groups need registers
-__host__ __device__ constexpr int dec_unroll(int ng) { return ng <= 2 ? 4 : 2; }
+__host__ __device__ constexpr int dec_unroll(int ng) { return ng == 1 ? 16 : ng == 2 ? 8 : 4; }
+
+// H' of one 64-row block as fixed-point digits with one exponent per token
+// and block: bmax holds each wave's per-token maxima of |hv|; lane (kg, r16)
+// holds rows rb*64 + wave*16 + kg*4 + i of token column r16 (lead lanes).
+template <int NG>
+__device__ __forceinline__ void write_h_digits(int R, int rb, int off, bool lead,
+                                               const bool (&bv)[NG], const float (&hv)[NG][4],
+                                               int8_t* __restrict__ hdig,
+                                               int32_t* __restrict__ hexp,
+                                               float (*bmax)[NG * kTokPerGroup]) {
+  const int nrb = R / kBlk;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kg = lane >> 4;
+  const int m = r16 / 3;
+  const int rbase = rb * kBlk + wave * 16 + kg * 4;
+  __syncthreads();
+#pragma unroll
+  for (int cg = 0; cg < NG; ++cg) {
+    if (!(lead && bv[cg])) continue;
+    const int ti = cg * kTokPerGroup + m;
+    const float mx = fmaxf(fmaxf(bmax[0][ti], bmax[1][ti]), fmaxf(bmax[2][ti], bmax[3][ti]));
+    const int Eh = kFixBits - exp_bound(mx);
+    uint32_t w0 = 0, w1 = 0, w2 = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int v = (int)rintf(ldexpf(hv[cg][i], Eh));
+      int d0, d1, d2;
+      split_digits(v, d0, d1, d2);
+      w0 |= (uint32_t)(d0 & 0xFF) << (8 * i);
+      w1 |= (uint32_t)(d1 & 0xFF) << (8 * i);
+      w2 |= (uint32_t)(d2 & 0xFF) << (8 * i);
+    }
+    const size_t pos = (size_t)off + ti;
+    int8_t* hp = hdig + pos * kDigits * R + rbase;
+    *(uint32_t*)(hp) = w0;
+    *(uint32_t*)(hp + R) = w1;
+    *(uint32_t*)(hp + 2 * (size_t)R) = w2;
+    if (wave == 0 && kg == 0) hexp[pos * nrb + rb] = Eh;
+  }
+}
 
 // Gate/up + SwiGLU of one block of 64 expert rows (rb) for the tokens of one
 // expert group, by a workgroup of 4 waves (wave w owns rows rb*64 + 16w ..
@@ -43,7 +84,6 @@ __device__ __forceinline__ void gateup_block(int C, int R, int rb, const int8_t*
                                              LoadB load_b, int8_t* __restrict__ hdig,
                                              int32_t* __restrict__ hexp,
                                              float (*bmax)[NG * kTokPerGroup]) {
-  const int nrb = R / kBlk;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kg = lane >> 4;
   const int m = r16 / 3, d = r16 - 3 * m;
@@ -61,7 +101,7 @@ __device__ __forceinline__ void gateup_block(int C, int R, int rb, const int8_t*
   const int nks = C / 64;
   struct Batch {
     v4i ag[kDecUnroll], au[kDecUnroll], b[kDecUnroll][NG];
-  } b0, b1;
+  };
   auto issue = [&](Batch& bt, int ks0) {
 #pragma unroll
     for (int u = 0; u < kDecUnroll; ++u) {
@@ -82,12 +122,13 @@ __device__ __forceinline__ void gateup_block(int C, int R, int rb, const int8_t*
         accu[cg] = mfma_i8(bt.au[u], bt.b[u][cg], accu[cg]);
       }
   };
-  issue(b0, 0);
-  for (int ks = 0; ks < nks; ks += 2 * kDecUnroll) {
-    issue(b1, ks + kDecUnroll);
-    consume(b0);
-    issue(b0, ks + 2 * kDecUnroll);
-    consume(b1);
+  // one batch per iteration, issued whole and consumed in order: no load
+  // result is carried around the loop, so the waits count down within the
+  // batch instead of draining at the back edge
+  for (int ks = 0; ks < nks; ks += kDecUnroll) {
+    Batch bt;
+    issue(bt, ks);
+    consume(bt);
   }
 
   // epilogue: rows rbase+i (i < 4) for token column r16
@@ -116,30 +157,161 @@ __device__ __forceinline__ void gateup_block(int C, int R, int rb, const int8_t*
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     if (kg == 0 && lead && r16 < 3 * kTokPerGroup) bmax[wave][cg * kTokPerGroup + m] = mx;
   }
-  __syncthreads();
+  write_h_digits<NG>(R, rb, off, lead, bv, hv, hdig, hexp, bmax);
+}
+
+// ---- INT4 variant (MIRA_FLAG_INT4) -----------------------------------------
+// 8 bytes of one 16-column run -> the int8 operand of those 16 columns, each
+// as 16*q: the run order puts columns 0-3 (8-11) in the high nibbles and
+// columns 4-7 (12-15) in the low nibbles of the first (second) dword.
+__device__ __forceinline__ v4i i4_operand(uint2 p) {
+  return v4i{(int)(p.x & 0xF0F0F0F0u), (int)((p.x << 4) & 0xF0F0F0F0u),
+             (int)(p.y & 0xF0F0F0F0u), (int)((p.y << 4) & 0xF0F0F0F0u)};
+}
+
+typedef unsigned int v2u __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint2 ld8_stream(const void* p) {
+  const v2u v = __builtin_nontemporal_load((const v2u*)p);
+  return uint2{v[0], v[1]};
+}
+
+// four fp16 scales (rows 4*kg .. 4*kg+3 of a tile) to fp32
+__device__ __forceinline__ void i4_scales(uint2 p, float (&s)[4]) {
+  s[0] = (float)__builtin_bit_cast(_Float16, (uint16_t)(p.x & 0xFFFFu));
+  s[1] = (float)__builtin_bit_cast(_Float16, (uint16_t)(p.x >> 16));
+  s[2] = (float)__builtin_bit_cast(_Float16, (uint16_t)(p.y & 0xFFFFu));
+  s[3] = (float)__builtin_bit_cast(_Float16, (uint16_t)(p.y >> 16));
+}
+
+// Float version of combine_digits_i for per-group scaled sums.
+__device__ __forceinline__ float combine_digits_f(float s0) {
+  const float s1 = __shfl_down(s0, 1, 64);
+  const float s2 = __shfl_down(s0, 2, 64);
+  return s2 * 65536.f + s1 * 256.f + s0;
+}
+
+// Gate/up + SwiGLU of one block of 64 expert rows for INT4 experts: the same
+// work split, operands and output as gateup_block.  Each k-step is one
+// 64-column group: the MFMA sums of that group are scaled by the group's
+// fp16 scale (per row) and accumulated in fp32; H' = silu(G) (.) U (no shared
+// scale to fold).  U k-steps per load batch; with B_AT_USE the activation
+// digits are read (from LDS) right before their MFMAs instead of travelling
+// with the weight loads, so a batch holds only weight registers.
+template <int NG, int U, bool B_AT_USE, typename LoadB>
+__device__ __forceinline__ void gateup_block_i4(int C, int R, int rb, const uint8_t* __restrict__ blob,
+                                                int off, const bool (&bv)[NG], const int (&xev)[NG],
+                                                LoadB load_b, int8_t* __restrict__ hdig,
+                                                int32_t* __restrict__ hexp,
+                                                float (*bmax)[NG * kTokPerGroup]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kg = lane >> 4;
+  const int m = r16 / 3, d = r16 - 3 * m;
+  const int nks = C / 64, npair = C / 128;
+  const int rtile = rb * (kBlk / 16) + wave;
+  // this wave's tile-row: nibble tiles of two groups (lane l's 16 bytes at
+  // 16*l) and the 32-byte scale blocks of its groups
+  const size_t mbytes = i4_matrix_bytes(R, C), nbytes = i4_nib_bytes(R, C);
+  const uint8_t* gq = blob + (size_t)rtile * npair * kI4PairTile + lane * 16;
+  const uint8_t* uq = gq + mbytes;
+  const uint8_t* gs = blob + nbytes + (size_t)rtile * nks * 32 + lane * 8;
+  const uint8_t* us = gs + mbytes;
+
+  float accg[NG][4], accu[NG][4];
+#pragma unroll
+  for (int cg = 0; cg < NG; ++cg)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) accg[cg][i] = accu[cg][i] = 0.f;
+
+  static_assert(U % 2 == 0 && U <= 16, "a batch covers whole tiles and one scale run");
+  constexpr int kDecUnroll = U;
+  struct Batch {
+    v4i qg[U / 2], qu[U / 2];  // two k-steps per 16-byte load
+    uint2 sg, su;              // lane l: group ks0 + l/4, rows 4*(l%4) .. +3
+    v4i b[B_AT_USE ? 1 : U][NG];
+    int ks0;
+  };
+  auto issue = [&](Batch& bt, int ks0) {
+#pragma unroll
+    for (int p = 0; p < U / 2; ++p) {
+      const int pair = ks0 / 2 + p;
+      const bool in = pair < npair;
+      bt.qg[p] = in ? ld16_stream(gq + (size_t)pair * kI4PairTile) : zero16();
+      bt.qu[p] = in ? ld16_stream(uq + (size_t)pair * kI4PairTile) : zero16();
+    }
+    const bool sin = (lane >> 2) < U && ks0 + (lane >> 2) < nks;
+    bt.sg = sin ? ld8_stream(gs + (size_t)ks0 * 32) : uint2{0, 0};
+    bt.su = sin ? ld8_stream(us + (size_t)ks0 * 32) : uint2{0, 0};
+    if constexpr (!B_AT_USE) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const bool in = ks0 + u < nks;
+#pragma unroll
+        for (int cg = 0; cg < NG; ++cg) bt.b[u][cg] = (in && bv[cg]) ? load_b(cg, ks0 + u) : zero16();
+      }
+    }
+    bt.ks0 = ks0;
+  };
+  auto consume = [&](const Batch& bt) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const v4i g2 = bt.qg[u / 2], u2 = bt.qu[u / 2];
+      const v4i ag = (u & 1) ? i4_operand(uint2{(uint32_t)g2[2], (uint32_t)g2[3]})
+                             : i4_operand(uint2{(uint32_t)g2[0], (uint32_t)g2[1]});
+      const v4i au = (u & 1) ? i4_operand(uint2{(uint32_t)u2[2], (uint32_t)u2[3]})
+                             : i4_operand(uint2{(uint32_t)u2[0], (uint32_t)u2[1]});
+      // this lane's four row scales of group ks0 + u sit in lane 4u + kg
+      float sgv[4], suv[4];
+      i4_scales(uint2{(uint32_t)__shfl((int)bt.sg.x, 4 * u + kg, 64),
+                      (uint32_t)__shfl((int)bt.sg.y, 4 * u + kg, 64)}, sgv);
+      i4_scales(uint2{(uint32_t)__shfl((int)bt.su.x, 4 * u + kg, 64),
+                      (uint32_t)__shfl((int)bt.su.y, 4 * u + kg, 64)}, suv);
+#pragma unroll
+      for (int cg = 0; cg < NG; ++cg) {
+        v4i bo;
+        if constexpr (B_AT_USE)
+          bo = bt.ks0 + u < nks ? load_b(cg, bt.ks0 + u) : zero16();
+        else
+          bo = bt.b[u][cg];
+        const v4i rg = mfma_i8(ag, bo, zero16());
+        const v4i ru = mfma_i8(au, bo, zero16());
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          accg[cg][i] = fmaf((float)rg[i], sgv[i], accg[cg][i]);
+          accu[cg][i] = fmaf((float)ru[i], suv[i], accu[cg][i]);
+        }
+      }
+    }
+  };
+  // one batch per iteration, issued whole and consumed in order: no load
+  // result is carried around the loop, so the waits count down within the
+  // batch instead of draining at the back edge
+  for (int ks = 0; ks < nks; ks += kDecUnroll) {
+    Batch bt;
+    issue(bt, ks);
+    consume(bt);
+  }
+
+  const bool lead = d == 0;
+  float hv[NG][4];
 #pragma unroll
   for (int cg = 0; cg < NG; ++cg) {
-    if (!(lead && bv[cg])) continue;
-    const int ti = cg * kTokPerGroup + m;
-    const float mx = fmaxf(fmaxf(bmax[0][ti], bmax[1][ti]), fmaxf(bmax[2][ti], bmax[3][ti]));
-    const int Eh = kFixBits - exp_bound(mx);
-    uint32_t w0 = 0, w1 = 0, w2 = 0;
+    // 2^-E of the token's fixed point, and 1/16 for the nibble operand (16*q)
+    const float xs = bv[cg] ? ldexpf(1.f, -xev[cg] - 4) : 0.f;
+    float mx = 0.f;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int v = (int)rintf(ldexpf(hv[cg][i], Eh));
-      int d0, d1, d2;
-      split_digits(v, d0, d1, d2);
-      w0 |= (uint32_t)(d0 & 0xFF) << (8 * i);
-      w1 |= (uint32_t)(d1 & 0xFF) << (8 * i);
-      w2 |= (uint32_t)(d2 & 0xFF) << (8 * i);
+      const float gv = combine_digits_f(accg[cg][i]) * xs;
+      const float uv = combine_digits_f(accu[cg][i]) * xs;
+      const float h = gv / (1.f + expf(-gv)) * uv;
+      hv[cg][i] = (lead && bv[cg]) ? h : 0.f;
+      mx = fmaxf(mx, fabsf(hv[cg][i]));
     }
-    const size_t pos = (size_t)off + ti;
-    int8_t* hp = hdig + pos * kDigits * R + rbase;
-    *(uint32_t*)(hp) = w0;
-    *(uint32_t*)(hp + R) = w1;
-    *(uint32_t*)(hp + 2 * (size_t)R) = w2;
-    if (wave == 0 && kg == 0) hexp[pos * nrb + rb] = Eh;
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    if (kg == 0 && lead && r16 < 3 * kTokPerGroup) bmax[wave][cg * kTokPerGroup + m] = mx;
   }
+  write_h_digits<NG>(R, rb, off, lead, bv, hv, hdig, hexp, bmax);
 }
 
 }  // namespace mira

@@ -17,6 +17,7 @@
 #include <vector>
 
 #include "mira.h"
+#include "int4_format.h"
 #include "mira_internal.h"
 
 namespace {
@@ -63,7 +64,8 @@ int check_shape(const mira_shape* s) {
                 MIRA_MAX_TOPK);
   if (s->act_dtype != MIRA_F32 && s->act_dtype != MIRA_BF16)
     return fail(MIRA_ERR_ARG, "act_dtype must be MIRA_F32 or MIRA_BF16");
-  const uint32_t known = MIRA_FLAG_SOFTMAX_ALL | MIRA_FLAG_FORCE_DECODE | MIRA_FLAG_FORCE_PREFILL;
+  const uint32_t known =
+      MIRA_FLAG_SOFTMAX_ALL | MIRA_FLAG_FORCE_DECODE | MIRA_FLAG_FORCE_PREFILL | MIRA_FLAG_INT4;
   if (s->flags & ~known) return fail(MIRA_ERR_ARG, "unknown flag bits 0x%x", s->flags & ~known);
   if ((s->flags & MIRA_FLAG_FORCE_DECODE) && (s->flags & MIRA_FLAG_FORCE_PREFILL))
     return fail(MIRA_ERR_ARG, "FORCE_DECODE and FORCE_PREFILL are exclusive");
@@ -78,7 +80,7 @@ bool decode_fits(const mira_shape& s, int T) {
 }
 
 bool use_decode(const mira_shape& s, int T) {
-  if (s.flags & MIRA_FLAG_FORCE_DECODE) return true;
+  if (s.flags & (MIRA_FLAG_FORCE_DECODE | MIRA_FLAG_INT4)) return true;
   if (s.flags & MIRA_FLAG_FORCE_PREFILL) return false;
   return decode_fits(s, T);
 }
@@ -94,6 +96,18 @@ int check_args(const mira_shape* s, const mira_moe_args* a, mira::Layout* L) {
                 "(got %d tokens)", MIRA_DECODE_MAX_TOKENS, mira::kDecodeMaxPairs, a->n_tokens);
   if ((int64_t)a->n_tokens * (s->top_k + s->n_shared) > (int64_t)1 << 30)
     return fail(MIRA_ERR_SHAPE, "too many tokens");
+  const bool i4 = s->flags & MIRA_FLAG_INT4;
+  if (i4 && (s->hidden % 128 || s->ffn % 128))
+    return fail(MIRA_ERR_SHAPE, "INT4 experts need hidden and ffn multiples of 128");
+  if (i4 && (s->flags & MIRA_FLAG_FORCE_PREFILL))
+    return fail(MIRA_ERR_UNSUPPORTED, "INT4 experts run on the decode kernels only");
+  if (i4 && !decode_fits(*s, a->n_tokens))
+    return fail(MIRA_ERR_UNSUPPORTED,
+                "INT4 experts run on the decode kernels only: n_tokens <= %d and n_tokens * "
+                "(top_k + n_shared) <= %d (got %d tokens)", MIRA_DECODE_MAX_TOKENS,
+                mira::kDecodeMaxPairs, a->n_tokens);
+  const size_t expert_bytes = i4 ? mira_packed_expert_bytes_int4(s->hidden, s->ffn)
+                                 : mira_packed_expert_bytes(s->hidden, s->ffn);
   *L = mira::make_layout(*s, a->n_tokens);
   if (a->n_tokens == 0) return MIRA_OK;
   if (!a->x || !a->w_router || !a->slot_table || !a->slot_pool || !a->out || !a->workspace)
@@ -103,9 +117,9 @@ int check_args(const mira_shape* s, const mira_moe_args* a, mira::Layout* L) {
     return fail(MIRA_ERR_ALIGN, "x, w_router and out must be 16-byte aligned");
   if (!aligned(a->slot_pool, 256) || a->slot_stride % 256)
     return fail(MIRA_ERR_ALIGN, "slot_pool and slot_stride must be 256-byte aligned");
-  if (a->slot_stride < mira_packed_expert_bytes(s->hidden, s->ffn))
+  if (a->slot_stride < expert_bytes)
     return fail(MIRA_ERR_SHAPE, "slot_stride %llu smaller than a packed expert (%zu bytes)",
-                (unsigned long long)a->slot_stride, mira_packed_expert_bytes(s->hidden, s->ffn));
+                (unsigned long long)a->slot_stride, expert_bytes);
   if (!aligned(a->workspace, 256)) return fail(MIRA_ERR_ALIGN, "workspace must be 256-byte aligned");
   if (a->workspace_bytes < L->total)
     return fail(MIRA_ERR_WORKSPACE, "workspace has %llu bytes, %zu needed for %d tokens",
@@ -274,6 +288,45 @@ hipEvent_t prof_event() {
   return e;
 }
 
+// INT4 variant, one (matrix, row) per work item; the same arithmetic as the
+// device packer (fp32 division, round half to even, fp16 scale rules).
+template <typename WT>
+void host_pack_one_i4(int C, int R, const WT* wg, const WT* wu, const WT* wd, float eps,
+                      uint8_t* blob, uint64_t stride) {
+  parallel_for((int64_t)2 * R + C, [&](int64_t b, int64_t e) {
+    for (int64_t it = b; it < e; ++it) {
+      const int mat = it < R ? 0 : it < 2 * R ? 1 : 2;
+      const int r = (int)(mat == 0 ? it : mat == 1 ? it - R : it - 2 * R);
+      const int K = mat == 2 ? R : C;
+      const WT* src = (mat == 0 ? wg : mat == 1 ? wu : wd) + (size_t)r * K;
+      uint8_t* m = blob + (size_t)mat * mira::i4_matrix_bytes(R, C);
+      for (int blk = 0; blk < K / 64; ++blk) {
+        float w[64], alpha = 0.f;
+        for (int c = 0; c < 64; ++c) {
+          w[c] = h_ld(src, (size_t)blk * 64 + c);
+          alpha = std::fmax(alpha, std::fabs(w[c]));
+        }
+        const uint16_t sb = mira::i4_scale_bits(std::fmax(alpha, eps) / (float)mira::kI4QMax);
+        const float sc = mira::i4_scale_value(sb);
+        auto q = [&](float v) {
+          const float t = std::rint(v / sc);
+          return (int)std::fmin(std::fmax(t, -(float)mira::kI4QMax), (float)mira::kI4QMax);
+        };
+        for (int gq = 0; gq < 4; ++gq) {
+          uint8_t* run = m + mira::i4_half_run_offset(r, blk, gq, K);
+          for (int bb = 0; bb < 8; ++bb) {
+            const int c = 16 * gq + 8 * (bb >> 2) + (bb & 3);
+            run[bb] = (uint8_t)(((q(w[c]) & 0xF) << 4) | (q(w[c + 4]) & 0xF));
+          }
+        }
+        std::memcpy(m + mira::i4_scale_offset(r, blk, mat == 2 ? C : R, K), &sb, 2);
+      }
+    }
+  });
+  const size_t used = 2 * mira::i4_matrix_bytes(R, C) + mira::i4_matrix_bytes(C, R);
+  std::memset(blob + used, 0, stride - used);
+}
+
 }  // namespace
 
 namespace mira {
@@ -330,6 +383,14 @@ int device_cu_count() {
 
 extern "C" {
 
+size_t mira_packed_expert_bytes_int4(int32_t hidden, int32_t ffn) {
+  if (hidden <= 0 || ffn <= 0 || hidden % 128 || ffn % 128) return 0;
+  const unsigned __int128 raw = (unsigned __int128)3 * hidden * ffn * 17 / 32;
+  const unsigned __int128 r = (raw + 255) / 256 * 256;
+  if (r > (unsigned __int128)SIZE_MAX) return 0;
+  return (size_t)r;
+}
+
 size_t mira_packed_expert_bytes(int32_t hidden, int32_t ffn) {
   if (hidden <= 0 || ffn <= 0) return 0;
   const unsigned __int128 raw = (unsigned __int128)3 * hidden * ffn + (unsigned __int128)2 * ffn;
@@ -353,7 +414,9 @@ int mira_pack_experts(const mira_shape* s, int32_t n_experts, int32_t w_dtype, c
   if (w_dtype != MIRA_F32 && w_dtype != MIRA_BF16) return fail(MIRA_ERR_ARG, "bad w_dtype");
   if (!(eps > 0.f) || !std::isfinite(eps)) return fail(MIRA_ERR_ARG, "eps must be positive and finite");
   if (on_device != 0 && on_device != 1) return fail(MIRA_ERR_ARG, "on_device must be 0 or 1");
-  const size_t need = mira_packed_expert_bytes(C, R);
+  const bool i4 = s->flags & MIRA_FLAG_INT4;
+  if (i4 && (C % 128 || R % 128)) return fail(MIRA_ERR_SHAPE, "INT4 packing needs hidden and ffn multiples of 128");
+  const size_t need = i4 ? mira_packed_expert_bytes_int4(C, R) : mira_packed_expert_bytes(C, R);
   if (need == 0) return fail(MIRA_ERR_SHAPE, "expert size overflows");
   if (packed_stride % 256 || packed_stride < need)
     return fail(MIRA_ERR_SHAPE, "packed_stride must be a multiple of 256 and >= %zu", need);
@@ -362,11 +425,28 @@ int mira_pack_experts(const mira_shape* s, int32_t n_experts, int32_t w_dtype, c
   const size_t esz = w_dtype == MIRA_F32 ? 4 : 2;
   if (on_device) {
     if (!aligned(packed, 256)) return fail(MIRA_ERR_ALIGN, "packed must be 256-byte aligned");
-    HIP_TRY(mira::launch_pack(C, R, n_experts, w_dtype, w_gate, w_up, w_down, eps, packed,
-                              packed_stride, stream));
+    if (i4)
+      HIP_TRY(mira::launch_pack_i4(C, R, n_experts, w_dtype, w_gate, w_up, w_down, eps, packed,
+                                   packed_stride, stream));
+    else
+      HIP_TRY(mira::launch_pack(C, R, n_experts, w_dtype, w_gate, w_up, w_down, eps, packed,
+                                packed_stride, stream));
     return ok();
   }
   const size_t per = (size_t)R * C;
+  if (i4) {
+    for (int e = 0; e < n_experts; ++e) {
+      uint8_t* blob = (uint8_t*)packed + (size_t)e * packed_stride;
+      if (w_dtype == MIRA_F32)
+        host_pack_one_i4<float>(C, R, (const float*)w_gate + e * per, (const float*)w_up + e * per,
+                                (const float*)w_down + e * per, eps, blob, packed_stride);
+      else
+        host_pack_one_i4<uint16_t>(C, R, (const uint16_t*)w_gate + e * per,
+                                   (const uint16_t*)w_up + e * per,
+                                   (const uint16_t*)w_down + e * per, eps, blob, packed_stride);
+    }
+    return ok();
+  }
   for (int e = 0; e < n_experts; ++e) {
     int8_t* blob = (int8_t*)packed + (size_t)e * packed_stride;
     if (w_dtype == MIRA_F32)

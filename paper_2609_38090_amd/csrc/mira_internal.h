@@ -222,10 +222,10 @@ hipError_t launch_decode_prep(const mira_shape& s, const Layout& L, const WsPtr&
                               hipStream_t st);
 hipError_t launch_decode(const mira_shape& s, const Layout& L, const WsPtr& w, const void* x,
                          const ExpertPool& ep, float* out, hipStream_t st);
-hipError_t launch_decode_down(const Layout& L, const WsPtr& w, const ExpertPool& ep, float* out,
-                              hipStream_t st);
 hipError_t launch_prefill(const mira_shape& s, const Layout& L, const WsPtr& w, const void* x,
                           const ExpertPool& ep, float* out, hipStream_t st);
+hipError_t launch_pack_i4(int C, int R, int n, int w_dtype, const void* wg, const void* wu,
+                          const void* wd, float eps, void* packed, uint64_t stride, hipStream_t st);
 hipError_t launch_pack(int C, int R, int n, int w_dtype, const void* wg, const void* wu,
                        const void* wd, float eps, void* packed, uint64_t stride, hipStream_t st);
 hipError_t launch_predict(const mira_pred_shape& p, const void* x, int T, const void* w1,

@@ -6,6 +6,7 @@
 // The division is the IEEE correctly rounded fp32 one (this file is built
 // without fast-math), so the bytes equal the host packer's.
 #include "device_util.h"
+#include "int4_format.h"
 #include "mira_internal.h"
 
 namespace mira {
@@ -100,6 +101,67 @@ __global__ __launch_bounds__(256) void pack_pad_kernel(int8_t* __restrict__ pack
   for (uint64_t i = used + (uint64_t)blockIdx.x * 256 + threadIdx.x; i < stride;
        i += (uint64_t)gridDim.x * 256)
     packed[(size_t)e * stride + i] = 0;
+}
+
+// INT4 variant: one thread per (row, group of 64 columns) of one matrix of one
+// expert; it owns the group's 32 nibble bytes (four 8-byte half-runs) and its
+// scale.
+template <typename WT>
+__global__ __launch_bounds__(256) void pack_i4_kernel(const WT* __restrict__ wg,
+                                                      const WT* __restrict__ wu,
+                                                      const WT* __restrict__ wd, int C, int R,
+                                                      float eps, uint8_t* __restrict__ packed,
+                                                      uint64_t stride) {
+  const int mat = blockIdx.y, e = blockIdx.z;
+  const int rows = mat == 2 ? C : R, K = mat == 2 ? R : C;
+  const int groups = K / 64;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)rows * groups) return;
+  const int r = (int)(idx / groups), blk = (int)(idx - (int64_t)r * groups);
+  const WT* src = (mat == 0 ? wg : mat == 1 ? wu : wd) + (size_t)e * R * C + (size_t)r * K + blk * 64;
+  float w[64];
+  float alpha = 0.f;
+#pragma unroll
+  for (int c = 0; c < 64; ++c) {
+    w[c] = ldw(src, c);
+    alpha = fmaxf(alpha, fabsf(w[c]));
+  }
+  const uint16_t sb = i4_scale_bits(fmaxf(alpha, eps) / (float)kI4QMax);
+  const float s = i4_scale_value(sb);
+  uint8_t* blob = packed + (size_t)e * stride + (size_t)mat * i4_matrix_bytes(R, C);  // gate, up, down
+#pragma unroll
+  for (int gq = 0; gq < 4; ++gq) {
+    uint64_t run = 0;
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const int c = 16 * gq + 8 * (b >> 2) + (b & 3);
+      const int qh = (int)fminf(fmaxf(rintf(w[c] / s), -(float)kI4QMax), (float)kI4QMax);
+      const int ql = (int)fminf(fmaxf(rintf(w[c + 4] / s), -(float)kI4QMax), (float)kI4QMax);
+      run |= (uint64_t)(((qh & 0xF) << 4) | (ql & 0xF)) << (8 * b);
+    }
+    *(uint64_t*)(blob + i4_half_run_offset(r, blk, gq, K)) = run;
+  }
+  *(uint16_t*)(blob + i4_scale_offset(r, blk, rows, K)) = sb;
+}
+
+hipError_t launch_pack_i4(int C, int R, int n, int w_dtype, const void* wg, const void* wu,
+                          const void* wd, float eps, void* packed, uint64_t stride,
+                          hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  prof_begin("pack", st);
+  const int64_t items = (int64_t)R * (C / 64);  // rows x groups, the same for all three matrices
+  const dim3 grid((unsigned)((items + 255) / 256), 3, n);
+  if (w_dtype == MIRA_BF16)
+    hipLaunchKernelGGL(pack_i4_kernel<uint16_t>, grid, dim3(256), 0, st, (const uint16_t*)wg,
+                       (const uint16_t*)wu, (const uint16_t*)wd, C, R, eps, (uint8_t*)packed, stride);
+  else
+    hipLaunchKernelGGL(pack_i4_kernel<float>, grid, dim3(256), 0, st, (const float*)wg,
+                       (const float*)wu, (const float*)wd, C, R, eps, (uint8_t*)packed, stride);
+  const uint64_t used = 2 * i4_matrix_bytes(R, C) + i4_matrix_bytes(C, R);
+  if (stride > used)
+    hipLaunchKernelGGL(pack_pad_kernel, dim3(64, n), dim3(256), 0, st, (int8_t*)packed, stride, used);
+  prof_end("pack", st);
+  return hipGetLastError();
 }
 
 hipError_t launch_pack(int C, int R, int n, int w_dtype, const void* wg, const void* wu,

@@ -42,16 +42,18 @@ class LazyBlobs:
 
     def __getitem__(self, e):
         if e not in self.cache:
-            self.cache[e] = oracle.pack_expert(*self.layer.master(e), eps=EPS)
+            self.cache[e] = self.layer.oracle_pack(*self.layer.master(e))
         return self.cache[e]
 
 
 class Layer:
     def __init__(self, cfg, layer=0, resident=None, spare_slots=0, T=None, slot_order=None,
-                 device="cuda"):
-        self.cfg, self.layer, self.device = cfg, layer, device
+                 device="cuda", fmt="int8"):
+        self.cfg, self.layer, self.device, self.fmt = cfg, layer, device, fmt
+        self.fflag = mira.MIRA_FLAG_INT4 if fmt == "int4" else 0
         self.T = cfg.T if T is None else T
-        self.stride = mira.mira_packed_expert_bytes(cfg.C, cfg.R)
+        self.stride = (mira.mira_packed_expert_bytes_int4(cfg.C, cfg.R) if fmt == "int4"
+                       else mira.mira_packed_expert_bytes(cfg.C, cfg.R))
         gd = gen_device(cfg)
         self.x = activations(cfg, layer, gd, T=self.T).to(device)
         self.wr = router_weights(cfg, layer, gd).to(device)
@@ -64,7 +66,7 @@ class Layer:
         self.n_slots = max(1, len(resident) + spare_slots)
         self.pool = torch.zeros(self.n_slots * self.stride, dtype=torch.uint8, device=device)
         table = [-1] * cfg.G
-        self.shape_pack = mira.MoEShape(cfg.C, cfg.R, 1, 1)
+        self.shape_pack = mira.MoEShape(cfg.C, cfg.R, 1, 1, flags=self.fflag)
         for slot, e in enumerate(resident):
             self.pack_into(e, slot)
             table[e] = slot
@@ -87,7 +89,7 @@ class Layer:
 
     def shape(self, flags=0):
         c = self.cfg
-        return mira.MoEShape(c.C, c.R, c.E, c.k, c.S, act_dtype(c), flags)
+        return mira.MoEShape(c.C, c.R, c.E, c.k, c.S, act_dtype(c), flags | self.fflag)
 
     def run(self, flags=0, two_phase=False, between=None):
         c, T, dev = self.cfg, self.T, self.device
@@ -127,9 +129,15 @@ class Layer:
         b = None if self.bias is None else self.bias.cpu().numpy().astype(np.float64)
         return x, wr, b
 
+    def oracle_pack(self, wg, wu, wd):
+        """The oracle's own packing of master weights, in this layer's format."""
+        if self.fmt == "int4":
+            return oracle.pack_expert_int4(wg, wu, wd, eps=EPS)
+        return oracle.pack_expert(wg, wu, wd, eps=EPS)
+
     def shared_blobs(self):
         c = self.cfg
-        return [oracle.pack_expert(*self.master(c.E + s), eps=EPS) for s in range(c.S)]
+        return [self.oracle_pack(*self.master(c.E + s)) for s in range(c.S)]
 
 
 def ffn_error(got, ref):
@@ -218,7 +226,8 @@ def run_and_check(lay, flags=0, tokens=None, res=None):
     plain = [t for t in tokens if t not in ties]
     ref = np.zeros((len(tokens), c.C))
     if plain:
-        o = oracle.moe_forward(o_x, o_wr, o_b, blobs, c.k, c.C, c.R, shared_blobs=shared, tokens=plain)
+        o = oracle.moe_forward(o_x, o_wr, o_b, blobs, c.k, c.C, c.R, shared_blobs=shared, tokens=plain,
+                               fmt=lay.fmt)
         for i, t in enumerate(plain):
             ref[tokens.index(t)] = o["out"][i]
     o_idx = oracle.topk_select(o_logits, c.k)
@@ -230,11 +239,11 @@ def run_and_check(lay, flags=0, tokens=None, res=None):
             alt = o_idx.copy()
             alt[t] = sorted(cand, key=lambda e: (-o_logits[t, e], e))
             o = oracle.moe_forward(o_x, o_wr, o_b, blobs, c.k, c.C, c.R, shared_blobs=shared,
-                                   idx=alt, tokens=[t])["out"][0]
+                                   idx=alt, tokens=[t], fmt=lay.fmt)["out"][0]
             err = np.linalg.norm(res["out"][t] - o)
             if best is None or err < best[0]:
                 best = (err, o)
         ref[tokens.index(t)] = best[1]
     got = res["out"][tokens]
-    errs = assert_ffn_close(got, ref, f"{c.name} flags={flags}")
+    errs = assert_ffn_close(got, ref, f"{c.name} {lay.fmt} flags={flags}")
     return res, errs, blobs, ties

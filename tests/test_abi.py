@@ -19,7 +19,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def _declared_functions():
     src = open(os.path.join(ROOT, "include", "mira.h")).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(mira_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(mira_[a-z0-9_]+)\s*\(", src)))
 
 
 def test_library_exports_every_declared_function():
@@ -170,3 +170,71 @@ def test_mixture_head_argument_checks():
         bad = mira.MixtureWeights(**{**w.__dict__, field: val})
         with pytest.raises(mira.MiraError):
             mira.mira_predict_mixture(good, bad, **args, stream=1)
+
+
+def _host_pack_i4(C, R, wg, wu, wd, dtype=mira.MIRA_F32, eps=1e-8, stride=None):
+    n = wg.shape[0]
+    stride = stride or oracle.packed_expert_bytes_int4(C, R)
+    out = np.full((n, stride), 0xAB, dtype=np.uint8)
+    mira.mira_pack_experts(mira.MoEShape(C, R, 1, 1, flags=mira.MIRA_FLAG_INT4), n, dtype, wg.ctypes.data,
+                           wu.ctypes.data, wd.ctypes.data, eps, out.ctypes.data, stride, 0)
+    return out
+
+
+def test_int4_packed_bytes_match_oracle():
+    for C, R in [(4096, 14336), (2048, 1408), (128, 128), (256, 512)]:
+        assert mira.mira_packed_expert_bytes_int4(C, R) == oracle.packed_expert_bytes_int4(C, R)
+    assert mira.mira_packed_expert_bytes_int4(0, 128) == 0
+    assert mira.mira_packed_expert_bytes_int4(64, 128) == 0     # the INT4 layout needs multiples of 128
+
+
+def test_host_pack_int4_matches_oracle():
+    """Random weights at three magnitudes (the smallest gives fp16 subnormal
+    scales), planted ties, all-zero and overflowing groups; fp32 and bf16."""
+    rng = np.random.default_rng(11)
+    C, R = 128, 256
+    w = [rng.standard_normal((3, *s)).astype(np.float32) for s in ((R, C), (R, C), (C, R))]
+    for t, scale in zip(w, (0.05, 1e-6, 3.0)):
+        t *= scale
+    w[0][0, 3, :64] = 0.0                       # an all-zero group
+    w[1][1, 5, 64:128] = 0.0
+    w[1][1, 5, 70] = 7e5                        # the scale saturates at 65504
+    w[0][2, 0, :6] = [7.0 * (1 + 2 ** -11), 3.5, 0.5, 1.5, 2.5, -3.5]   # ties
+    w[0][2, 0, 6:64] = 0.0
+    stride = oracle.packed_expert_bytes_int4(C, R) + 256
+    got = _host_pack_i4(C, R, *w, stride=stride)
+    for e in range(3):
+        ref = oracle.pack_expert_int4(w[0][e], w[1][e], w[2][e])
+        assert np.array_equal(got[e, :ref.size], ref), e
+        assert not got[e, ref.size:].any()
+    wb = [torch.from_numpy(t).to(torch.bfloat16) for t in w]
+    bits = [t.view(torch.int16).numpy().view(np.uint16).copy() for t in wb]
+    got = _host_pack_i4(C, R, *bits, dtype=mira.MIRA_BF16)
+    for e in range(3):
+        assert np.array_equal(got[e], oracle.pack_expert_int4(*(t[e].float().numpy() for t in wb))), e
+
+
+def test_int4_forward_argument_checks():
+    C, R = 256, 512
+    s = mira.MoEShape(C, R, 4, 2, 0, mira.MIRA_F32, flags=mira.MIRA_FLAG_INT4)
+    ws = mira.mira_workspace_bytes(s, 16)
+    base = dict(x=0x1000, n_tokens=4, n_slots=4, w_router=0x2000, slot_table=0x3000, slot_pool=0x10000,
+                slot_stride=oracle.packed_expert_bytes_int4(C, R), out=0x4000, workspace=0x20000,
+                workspace_bytes=ws)
+    for shape_flags, change, code in [
+            (mira.MIRA_FLAG_INT4 | mira.MIRA_FLAG_FORCE_PREFILL, {}, -6),
+            (mira.MIRA_FLAG_INT4, dict(n_tokens=17), -6),
+            (mira.MIRA_FLAG_INT4, dict(slot_stride=oracle.packed_expert_bytes_int4(C, R) - 256), -2)]:
+        sh = mira.MoEShape(C, R, 4, 2, 0, mira.MIRA_F32, flags=shape_flags)
+        with pytest.raises(mira.MiraError) as ei:
+            mira.mira_moe_forward(sh, mira.MoEArgs(**dict(base, **change)), stream=1)
+        assert ei.value.code == code, (shape_flags, change)
+    for hidden, ffn in [(192, 512), (256, 448)]:   # INT4 needs multiples of 128
+        sh = mira.MoEShape(hidden, ffn, 4, 2, 0, mira.MIRA_F32, flags=mira.MIRA_FLAG_INT4)
+        with pytest.raises(mira.MiraError) as ei:
+            mira.mira_moe_forward(sh, mira.MoEArgs(**base), stream=1)
+        assert ei.value.code == -2
+        with pytest.raises(mira.MiraError):
+            _host_pack_i4(hidden, ffn, *(np.zeros((1, *sh_), dtype=np.float32)
+                                         for sh_ in ((ffn, hidden), (ffn, hidden), (hidden, ffn))),
+                          stride=256 * 1024)

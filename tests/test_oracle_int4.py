@@ -25,14 +25,16 @@ def _grid_int4(rng, rows, K):
 
 
 def test_packed_bytes_closed_form():
-    assert oracle.packed_expert_bytes_int4(4096, 14336) == 3 * 896 * 64 * 544   # already a multiple of 256
-    assert oracle.packed_expert_bytes_int4(64, 64) == 6656                      # 3*4*544 = 6528 -> 6656
+    # per matrix rows*K/2 nibble bytes + rows*K/64 fp16 scales = rows*K*17/32
+    assert oracle.packed_expert_bytes_int4(4096, 14336) == 3 * 4096 * 14336 * 17 // 32
+    assert oracle.packed_expert_bytes_int4(128, 128) == 26112                   # 3*8704, a multiple of 256
+    assert oracle.packed_expert_bytes_int4(128, 384) == 78336                   # multiples of 128 never need padding
     assert oracle.packed_expert_bytes_int4(256, 512) % 256 == 0
 
 
 def test_grid_weights_round_trip_exactly():
     rng = np.random.default_rng(0)
-    C, R = 128, 64
+    C, R = 256, 128
     (qg, sg, wg), (qu, su, wu) = _grid_int4(rng, R, C), _grid_int4(rng, R, C)
     qd, sd, wd = _grid_int4(rng, C, R)
     blob = oracle.pack_expert_int4(wg, wu, wd)
@@ -47,32 +49,34 @@ def test_grid_weights_round_trip_exactly():
 
 
 def test_layout_places_one_element_by_the_formula():
-    # q[5, 64 + 16*2 + 8 + 4 + 1] = 3: tile (tile-row 0, block 1), run g*16 + i
-    # with g = 2, i = 5, byte b = 4*1 + 1 = 5, low nibble (the +4 half).
-    rows, K = 16, 128
+    # q[5, 128 + 64 + 16*2 + 8 + 4 + 1] = 3: nibble tile (tile-row 0, column
+    # pair 1), second group of the pair (bytes 8..15 of the run), run g*16 + i
+    # with g = 2, i = 5, byte b = 4*1 + 1 = 5, low nibble (the +4 half):
+    # offset 1024 + (2*16 + 5)*16 + 8 + 5.
+    rows, K = 16, 256
     q = np.zeros((rows, K), dtype=np.int8)
-    q[5, 64 + 32 + 8 + 4 + 1] = 3
+    q[5, 128 + 64 + 32 + 8 + 4 + 1] = 3
     q[0, 0] = -1        # tile 0, run 0, byte 0, high nibble
     s = np.full((rows, K // 64), 1.0, dtype=np.float16)
-    s[9, 1] = 0.5
+    s[9, 3] = 0.5       # scale region at rows*K/2 = 2048: group 3, row 9 -> 2048 + 3*32 + 2*9
     flat = oracle.int4_tile_order(q, s)
-    assert flat.size == 2 * 544
-    expect = np.zeros(2 * 544, dtype=np.uint8)
+    assert flat.size == 2048 + 16 * 4 * 2
+    expect = np.zeros(flat.size, dtype=np.uint8)
     expect[0] = 0xF0
-    expect[544 + (2 * 16 + 5) * 8 + 5] = 0x03
+    expect[1024 + (2 * 16 + 5) * 16 + 8 + 5] = 0x03
     one, half = np.float16(1.0).view(np.uint16), np.float16(0.5).view(np.uint16)
-    for t in range(2):
+    for grp in range(4):
         for i in range(16):
-            v = half if (t, i) == (1, 9) else one
-            expect[t * 544 + 512 + 2 * i] = v & 0xFF
-            expect[t * 544 + 512 + 2 * i + 1] = v >> 8
+            v = half if (grp, i) == (3, 9) else one
+            expect[2048 + grp * 32 + 2 * i] = v & 0xFF
+            expect[2048 + grp * 32 + 2 * i + 1] = v >> 8
     assert np.array_equal(flat, expect)
     q2, s2 = oracle.int4_untile_order(flat, rows, K)
     assert np.array_equal(q2, q) and np.array_equal(s2, s)
 
 
 def _one_group(vals):
-    w = np.zeros((64, 64), dtype=np.float32)
+    w = np.zeros((128, 128), dtype=np.float32)
     w[0, :len(vals)] = vals
     return w
 
@@ -91,7 +95,7 @@ def test_scale_ties_to_even_and_integers_use_the_stored_scale():
 
 def _pack_matrix(w):
     """Quantize one matrix the way pack_expert_int4 does (through the public
-    packer: the matrix is the gate of an expert with C = R = 64)."""
+    packer: the matrix is the gate of an expert with C = R = 128)."""
     C, R = w.shape[1], w.shape[0]
     blob = oracle.pack_expert_int4(w, np.zeros_like(w), np.zeros((C, R), dtype=np.float32))
     (q, s), _, _ = oracle.unpack_expert_int4(blob, C, R)
@@ -99,7 +103,7 @@ def _pack_matrix(w):
 
 
 def test_degenerate_groups():
-    C, R = 64, 64
+    C, R = 128, 128
     w = np.zeros((R, C), dtype=np.float32)
     w[1, 3] = 1e6          # alpha / 7 overflows fp16 -> 65504; 1e6 / 65504 -> 15 -> clamp 7
     w[2, 0] = -1e-9        # alpha below eps: eps / 7 = 1.4e-9 rounds to fp16 zero -> 2^-24
@@ -112,16 +116,16 @@ def test_degenerate_groups():
 
 def test_rejects_bad_shapes():
     with pytest.raises(ValueError):
-        oracle.pack_expert_int4(np.zeros((16, 64)), np.zeros((16, 64)), np.zeros((64, 16)))
+        oracle.pack_expert_int4(np.zeros((64, 128)), np.zeros((64, 128)), np.zeros((128, 64)))
     with pytest.raises(ValueError):
-        oracle.int4_tile_order(np.zeros((8, 64), dtype=np.int8), np.zeros((8, 1)))
+        oracle.int4_tile_order(np.zeros((16, 64), dtype=np.int8), np.zeros((16, 1)))
 
 
 def test_int4_ffn_uses_the_dequantized_weights():
     # With grid weights the INT4 blob dequantizes to the exact weights, so the
     # expert output equals the SwiGLU of those weights computed directly.
     rng = np.random.default_rng(3)
-    C, R = 64, 64
+    C, R = 128, 128
     _, _, wg = _grid_int4(rng, R, C)
     _, _, wu = _grid_int4(rng, R, C)
     _, _, wd = _grid_int4(rng, C, R)
