@@ -42,10 +42,12 @@ COLD_BYTES = 1 << 30
 # shared headers); otherwise the bench reports traffic as null.
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 TRAFFIC = {
-    ("decode_gateup", "mixtral_decode"): dict(sources=("decode.hip", "decode_dev.h"), sha="ae857e8dd1f46f20",
-                                               fetch_kib=114811.3, write_kib=98.0),
-    ("prefill_gateup", "mixtral_prefill"): dict(sources=("prefill.hip",), sha="3e60b10b4e04359c",
-                                                 fetch_kib=601387.7, write_kib=38177.1),
+    ("decode_gateup", "mixtral_decode"): dict(sources=("decode.hip", "decode_dev.h", "int4_format.h"),
+                                               sha="e6d1a726c71d3fa1", fetch_kib=114817.3, write_kib=98.0),
+    ("decode_gateup", "mixtral_decode_int4"): dict(sources=("decode.hip", "decode_dev.h", "int4_format.h"),
+                                                    sha="e6d1a726c71d3fa1", fetch_kib=61050.9, write_kib=98.0),
+    ("prefill_gateup", "mixtral_prefill"): dict(sources=("prefill.hip",), sha="e127507f028c6924",
+                                                 fetch_kib=602308.2, write_kib=38289.3),
 }
 
 
