@@ -292,20 +292,22 @@ def cpu_baseline(cfg, copy0, budget_s, fmt="int8"):
     }
 
 
-def build_stack(cfg, n_layers, n_stage, hot=None, bias=None, host_all=False, rebalancer=None):
+def build_stack(cfg, n_layers, n_stage, hot=None, bias=None, host_all=False, rebalancer=None,
+                fmt="int8"):
     """The beam workload's stack: per layer its seeded input, router, HOT experts
     packed into their device slots and the other experts (all of them if
     host_all, as a rebalancer may evict and later promote any expert) packed
     into pinned host memory, one blob each, plus the predictor head scoring
-    layer l+2.  hot(l) and bias(l) override the workload's HOT set and bias."""
+    layer l+2.  hot(l) and bias(l) override the workload's HOT set and bias;
+    fmt picks the expert format ("int8" or the "int4" variant)."""
     import torch
     import paper_2609_38090_amd as mira
     from paper_2609_38090_amd.stack import ExpertStack, LayerData
     from mira_inputs import (activations, expert_weights, predictor_weights, resident_experts,
                              router_bias, router_weights)
 
-    stride = mira.mira_packed_expert_bytes(cfg.C, cfg.R)
-    pack_shape = mira.MoEShape(cfg.C, cfg.R, 1, 1)
+    stride = expert_stride(cfg, fmt)
+    pack_shape = mira.MoEShape(cfg.C, cfg.R, 1, 1, flags=format_flag(fmt))
     layers = []
     for l in range(n_layers):
         b = router_bias(cfg, l) if bias is None else bias(l)
@@ -313,7 +315,7 @@ def build_stack(cfg, n_layers, n_stage, hot=None, bias=None, host_all=False, reb
         layers.append(LayerData(x=activations(cfg, l, "cuda"), w_router=router_weights(cfg, l, "cuda"),
                                 bias=None if b is None else b.cuda(),
                                 hot=resident_experts(cfg, l) if hot is None else hot(l), pred=pred))
-    shape = mira.MoEShape(cfg.C, cfg.R, cfg.E, cfg.k, cfg.S, mira.MIRA_BF16, 0)
+    shape = mira.MoEShape(cfg.C, cfg.R, cfg.E, cfg.k, cfg.S, mira.MIRA_BF16, format_flag(fmt))
     ps = mira.PredShape(cfg.C, cfg.pred_hidden, cfg.E, cfg.pred_group, mira.MIRA_BF16)
     stack = ExpertStack(shape, cfg.T, layers, stride, n_stage=n_stage, pred_shape=ps, rebalancer=rebalancer)
     n_host = sum(cfg.E if host_all else cfg.E - len(ld.hot) for ld in layers)
@@ -338,7 +340,7 @@ def build_stack(cfg, n_layers, n_stage, hot=None, bias=None, host_all=False, reb
     return stack, stride
 
 
-def run_drift(cfg, n_layers, steps, period):
+def run_drift(cfg, n_layers, steps, period, fmt="int8"):
     """HOT rebalancing on a workload whose expert popularity drifts: every
     `period` steps the Zipf ranks of every layer's router bias change.  The
     same inputs run with a static HOT set (the popular experts of the first
@@ -354,7 +356,8 @@ def run_drift(cfg, n_layers, steps, period):
         rb = Rebalancer(RebalanceConfig(interval=64, max_swaps=1, probation=2)) if name == "rebalanced" else None
         stack, _ = build_stack(cfg, n_layers, max(cfg.E - cfg.resident, 4) + 2,
                                hot=lambda l: drift_hot(cfg, l, 0, cfg.resident),
-                               bias=lambda l: drift_bias(cfg, l, 0), host_all=True, rebalancer=rb)
+                               bias=lambda l: drift_bias(cfg, l, 0), host_all=True, rebalancer=rb,
+                               fmt=fmt)
         per_epoch = []
         t0 = time.perf_counter()
         for s in range(steps):
@@ -470,7 +473,8 @@ def run_stack(args, cfg):
     mira.load()
     L = args.layers or cfg.layers
     t_build = time.perf_counter()
-    stack, stride = build_stack(cfg, L, args.stage_slots)
+    fmt = args.format
+    stack, stride = build_stack(cfg, L, args.stage_slots, fmt=fmt)
     build_s = time.perf_counter() - t_build
     # the true routing of every layer (the oracle-prefetch mode stages it)
     true_idx, active = [], []
@@ -535,7 +539,7 @@ def run_stack(args, cfg):
     stack.set_predictor(mlp_shape, heads_mlp)
     heads = run_heads(cfg, L - 2, stack, heads_mix, mix_shape)
     ms = modes["predict"]["ms_per_step"]
-    gu_bytes = sum(a * (2 * cfg.R * cfg.C + 2 * cfg.R) for a in active) / L
+    gu_bytes = sum(algorithmic_units(cfg, [1] * a + [0] * (cfg.G - a), fmt)["gu_bytes"] for a in active) / L
     roof = None
     cnt, tot_ms = prof.get("decode_gateup", (0, 0.0))
     if cnt:
@@ -549,7 +553,7 @@ def run_stack(args, cfg):
         "metric": METRIC, "value": modes["predict"]["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1,
         "steps": steps, "warmup": warm, "ms_per_step": ms, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "i8", "data": "synthetic",
-        "config": {"workload": cfg.name, "tokens": cfg.T, "layers": L, "hidden": cfg.C,
+        "config": {"workload": cfg.name, "format": fmt, "tokens": cfg.T, "layers": L, "hidden": cfg.C,
                    "experts": cfg.E, "top_k": cfg.k, "ffn": cfg.R, "resident_per_layer": cfg.resident,
                    "stage_slots": args.stage_slots, "predictor": f"{cfg.C}->{cfg.pred_hidden}->{cfg.E}",
                    "activations": cfg.act, "experts_selected_per_layer": round(sum(active) / L, 2)},
@@ -562,10 +566,11 @@ def run_stack(args, cfg):
         "roofline": roof,
     }
     if args.drift_steps > 0:
-        line["drift"] = run_drift(cfg, min(L, 8), args.drift_steps, max(1, args.drift_steps // 3))
+        line["drift"] = run_drift(cfg, min(L, 8), args.drift_steps, max(1, args.drift_steps // 3), fmt)
     if not args.no_cpu_baseline:
         ld = stack.layers[0]
-        line["cpu_baseline"] = cpu_baseline(cfg, dict(x=ld.x, wr=ld.w_router, bias=ld.bias), args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(cfg, dict(x=ld.x, wr=ld.w_router, bias=ld.bias), args.cpu_seconds,
+                                            fmt)
     print(json.dumps(line), flush=True)
     return 0
 
@@ -596,9 +601,9 @@ def main():
     mira.load()
     cfg = CONFIGS[args.workload]
     fmt = args.format
-    if fmt == "int4" and (cfg.layers > 1 or cfg.T > mira.MIRA_DECODE_MAX_TOKENS):
-        print(json.dumps({"error": "the INT4 variant runs on the decode kernels: use a single-layer "
-                                   "decode workload (mixtral_decode, tiny)", "workload": cfg.name}))
+    if fmt == "int4" and cfg.T > mira.MIRA_DECODE_MAX_TOKENS:
+        print(json.dumps({"error": "the INT4 variant runs on the decode kernels: use a decode "
+                                   "workload (mixtral_decode, beam_stack, tiny)", "workload": cfg.name}))
         return 2
     if cfg.layers > 1:
         return run_stack(args, cfg)

@@ -17,6 +17,9 @@ MIX_PA, MIX_PH = 48, 16  # MixtureHead widths of the small stack
 
 SMALL_STACK = MoEConfig("small_stack", 104, T=8, C=128, E=8, k=2, R=192, zipf_s=1.2, layers=5, resident=4,
                         pred_hidden=32, pred_group=8)
+# the INT4 layout needs hidden and ffn multiples of 128
+SMALL_STACK_I4 = MoEConfig("small_stack_i4", 105, T=8, C=128, E=8, k=2, R=256, zipf_s=1.2, layers=5,
+                           resident=4, pred_hidden=32, pred_group=8)
 
 
 def _head(mira, cfg, l, head):
@@ -28,9 +31,12 @@ def _head(mira, cfg, l, head):
     return mira.MixtureWeights(**{k: v.cuda() for k, v in W.items() if torch.is_tensor(v)}, bg=W["bg"])
 
 
-def build(mira, cfg, n_stage, hot=None, bias=None, host_all=False, rebalancer=None, head="mlp"):
+def build(mira, cfg, n_stage, hot=None, bias=None, host_all=False, rebalancer=None, head="mlp",
+          fmt="int8"):
     from paper_2609_38090_amd.stack import ExpertStack, LayerData
-    stride = mira.mira_packed_expert_bytes(cfg.C, cfg.R)
+    i4 = fmt == "int4"
+    flag = mira.MIRA_FLAG_INT4 if i4 else 0
+    stride = (mira.mira_packed_expert_bytes_int4 if i4 else mira.mira_packed_expert_bytes)(cfg.C, cfg.R)
     layers, blobs = [], {}
     for l in range(cfg.layers):
         b = router_bias(cfg, l) if bias is None else bias(l)
@@ -38,15 +44,16 @@ def build(mira, cfg, n_stage, hot=None, bias=None, host_all=False, rebalancer=No
         layers.append(LayerData(x=activations(cfg, l, "cuda"), w_router=router_weights(cfg, l, "cuda"),
                                 bias=None if b is None else b.cuda(),
                                 hot=resident_experts(cfg, l) if hot is None else hot(l), pred=pred))
-    shape = mira.MoEShape(cfg.C, cfg.R, cfg.E, cfg.k, cfg.S, mira.MIRA_BF16, 0)
+    shape = mira.MoEShape(cfg.C, cfg.R, cfg.E, cfg.k, cfg.S, mira.MIRA_BF16, flag)
     ps = (mira.PredShape(cfg.C, cfg.pred_hidden, cfg.E, cfg.pred_group, mira.MIRA_BF16) if head == "mlp" else
           mira.MixtureShape(cfg.C, cfg.E, cfg.k, cfg.k, MIX_PA, MIX_PH, cfg.E, cfg.pred_group, mira.MIRA_BF16))
     st = ExpertStack(shape, cfg.T, layers, stride, n_stage=n_stage, pred_shape=ps, rebalancer=rebalancer)
-    pack_shape = mira.MoEShape(cfg.C, cfg.R, 1, 1)
+    pack_shape = mira.MoEShape(cfg.C, cfg.R, 1, 1, flags=flag)
     for l, ld in enumerate(layers):
         for e in range(cfg.E):
             w = [np.ascontiguousarray(t.numpy()) for t in expert_weights(cfg, l, e, "cpu")]
-            blobs[l, e] = oracle.pack_expert(*w, eps=EPS)  # the oracle's own packing, for the reference
+            # the oracle's own packing, for the reference
+            blobs[l, e] = (oracle.pack_expert_int4 if i4 else oracle.pack_expert)(*w, eps=EPS)
             pinned = torch.zeros(stride, dtype=torch.uint8).pin_memory()
             mira.mira_pack_experts(pack_shape, 1, mira.MIRA_F32, w[0].ctypes.data, w[1].ctypes.data,
                                    w[2].ctypes.data, EPS, pinned, stride, 0)
@@ -69,10 +76,10 @@ def run(st, mode, true_idx=None):
     return {l: o.cpu().numpy() for l, o in outs.items()}, stats
 
 
-@pytest.mark.parametrize("n_stage", [4, 8])
-def test_stack_modes_agree_and_match_oracle(mira, n_stage):
-    cfg = SMALL_STACK
-    st, blobs = build(mira, cfg, n_stage)
+@pytest.mark.parametrize("n_stage,fmt", [(4, "int8"), (8, "int8"), (4, "int4")])
+def test_stack_modes_agree_and_match_oracle(mira, n_stage, fmt):
+    cfg = SMALL_STACK if fmt == "int8" else SMALL_STACK_I4
+    st, blobs = build(mira, cfg, n_stage, fmt=fmt)
     true_idx = []
     for l in range(cfg.layers):
         mira.mira_moe_route(st.shape, st.args(l))
@@ -102,7 +109,7 @@ def test_stack_modes_agree_and_match_oracle(mira, n_stage):
         x = ld.x.float().cpu().numpy().astype(np.float64)
         wr = ld.w_router.float().cpu().numpy().astype(np.float64)
         b = None if ld.bias is None else ld.bias.cpu().numpy().astype(np.float64)
-        ref = oracle.moe_forward(x, wr, b, [blobs[l, e] for e in range(cfg.E)], cfg.k, cfg.C, cfg.R)
+        ref = oracle.moe_forward(x, wr, b, [blobs[l, e] for e in range(cfg.E)], cfg.k, cfg.C, cfg.R, fmt=fmt)
         assert np.array_equal(ref["idx"], true_idx[l])
         assert_ffn_close(base[l], ref["out"], f"stack layer {l}")
 
