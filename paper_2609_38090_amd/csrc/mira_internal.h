@@ -44,7 +44,7 @@ struct Layout {
   int mt_max;   // upper bound of prefill m-tiles
   int ksplit;   // most k-chunks of the prefill down GEMM (partials summed in order by the combine)
   size_t logits, idx, wts, counts, offsets, inv, tokpos, wpos, misc, active, mstart, pcnt,
-      dwork, xdig, xexp, hdig, hexp, xb16, hbuf, ybuf, total;
+      dwork, xdig, hdig, hexp, xb16, hbuf, ybuf, total;
 };
 
 // One non-empty expert group of a decode call, written by the decode
@@ -119,7 +119,6 @@ inline Layout make_layout(const mira_shape& s, int T) {
   L.pcnt = take((size_t)kPermChunkMax * L.E * 4);
   L.dwork = take(G * sizeof(DecodeWork));
   L.xdig = take((size_t)L.Td * kDigits * L.C);
-  L.xexp = take((size_t)L.Td * 4);
   L.hdig = take((size_t)L.Pd * kDigits * L.R);
   L.hexp = take((size_t)L.Pd * (L.R / kBlk) * 4);
   L.xb16 = take(s.act_dtype == MIRA_F32 ? Tz * L.C * 2 : 0);
@@ -145,7 +144,6 @@ struct WsPtr {
   int32_t* pcnt;
   DecodeWork* dwork;
   int8_t* xdig;
-  int32_t* xexp;
   int8_t* hdig;
   int32_t* hexp;
   uint16_t* xb16;
@@ -170,7 +168,6 @@ inline WsPtr ws_ptrs(const Layout& L, void* base) {
   w.pcnt = (int32_t*)(b + L.pcnt);
   w.dwork = (DecodeWork*)(b + L.dwork);
   w.xdig = (int8_t*)(b + L.xdig);
-  w.xexp = (int32_t*)(b + L.xexp);
   w.hdig = (int8_t*)(b + L.hdig);
   w.hexp = (int32_t*)(b + L.hexp);
   w.xb16 = (uint16_t*)(b + L.xb16);

@@ -349,16 +349,18 @@ __global__ __launch_bounds__(kBigThreads) void permute_kernel(const int32_t* __r
 // ---------------------------------------------------------------------------
 // Decode preparation (T <= 16 tokens, one workgroup): router logits (with
 // max |x| per token on the way), top-k and weights; then wave 0 groups the
-// pairs while the other waves write the fixed-point digits of x used by the
+// pairs (with wave 1 writing the optional outputs when there are at most 64
+// pairs) while the other waves write the fixed-point digits of x used by the
 // integer expert kernels (|x * 2^E_t| < 2^22 per token, three signed
-// base-256 digits; layout xdig[(t*3 + d)*C + c], xexp[t] = E_t).
+// base-256 digits; layout xdig[(t*3 + d)*C + c]; the exponent E_t goes into
+// the expert descriptors).
 // ---------------------------------------------------------------------------
 template <typename ActT>
 __global__ __launch_bounds__(kBigThreads) void decode_prep_kernel(
     const ActT* __restrict__ x, const ActT* __restrict__ wr, const float* __restrict__ bias,
     int T, int E, int C, int k, int S, int softmax_all, float* __restrict__ logits_out,
     ExpertPool ep, PermOut o, DecodeWork* __restrict__ work, int max_active,
-    int8_t* __restrict__ xdig, int32_t* __restrict__ xexp) {
+    int8_t* __restrict__ xdig) {
   __shared__ float lg[kRouteTok][MIRA_MAX_EXPERTS];
   __shared__ float part[kBigWaves][16][17];
   __shared__ int32_t idx_s[kRouteTok * MIRA_MAX_TOPK];
@@ -415,21 +417,28 @@ __global__ __launch_bounds__(kBigThreads) void decode_prep_kernel(
       for (int e = lane; e < E; e += 64) logits_out[(size_t)t * E + e] = lg[t][e];
     topk_rank(lg[t], E, k, softmax_all, idx_s + t * k, w_s + t * k, sel_e[t], sel_v[t]);
   }
-  if (tid < T) {
-    const int Ex = kFixBits - exp_bound(xmax[tid]);
-    xe_s[tid] = Ex;
-    xexp[tid] = Ex;
-  }
-  __syncthreads();
+  if (tid < T) xe_s[tid] = kFixBits - exp_bound(xmax[tid]);
+  lds_barrier();  // the routing and exponents are in LDS; no global data is read after this
 
+  // up to 64 pairs: wave 0 writes the expert kernels' descriptors and wave 1
+  // the optional outputs side by side; otherwise wave 0 does both
+  const bool small = T * k <= kDecodeSmallPairs;
   if (wave == 0) {
-    permute_decode_wave(idx_s, w_s, xe_s, slot_s, T, k, E, S, ep, o, work, max_active, cnt_s,
-                        run_s, ptok_s, pw_s);
+    if (small)
+      decode_work_small(idx_s, w_s, xe_s, slot_s, T, k, E, S, ep, work, max_active);
+    else
+      permute_decode_wave(idx_s, w_s, xe_s, slot_s, T, k, E, S, ep, o, work, max_active, cnt_s,
+                          run_s, ptok_s, pw_s);
     return;
   }
-  // waves 1..15: fixed-point digits of x, four elements per thread and step
+  if (small && wave == 1) {
+    decode_outputs_small(idx_s, w_s, T, k, E, S, o, cnt_s);
+    return;
+  }
+  // the other waves: fixed-point digits of x, four elements per thread and step
+  const int w0d = small ? 2 : 1;
   const int q4 = C / 4, n4 = T * q4;
-  for (int i = tid - 64; i < n4; i += kBigThreads - 64) {
+  for (int i = tid - 64 * w0d; i < n4; i += kBigThreads - 64 * w0d) {
     const int t = i / q4, c = (i - t * q4) * 4;
     const int Ex = xe_s[t];
     float v[4];
@@ -503,11 +512,11 @@ hipError_t launch_decode_prep(const mira_shape& s, const Layout& L, const WsPtr&
   if (s.act_dtype == MIRA_BF16)
     hipLaunchKernelGGL(decode_prep_kernel<uint16_t>, dim3(1), dim3(kBigThreads), 0, st,
                        (const uint16_t*)x, (const uint16_t*)wr, bias, L.T, L.E, L.C, L.k, L.S, sa,
-                       logits_out, ep, o, w.dwork, max_active, w.xdig, w.xexp);
+                       logits_out, ep, o, w.dwork, max_active, w.xdig);
   else
     hipLaunchKernelGGL(decode_prep_kernel<float>, dim3(1), dim3(kBigThreads), 0, st,
                        (const float*)x, (const float*)wr, bias, L.T, L.E, L.C, L.k, L.S, sa,
-                       logits_out, ep, o, w.dwork, max_active, w.xdig, w.xexp);
+                       logits_out, ep, o, w.dwork, max_active, w.xdig);
   prof_end("decode_prep", st);
   return hipGetLastError();
 }

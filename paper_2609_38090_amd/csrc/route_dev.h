@@ -151,6 +151,38 @@ __device__ __forceinline__ void topk_rank(const float* lgrow, int E, int k, int 
                                           int32_t* idx_a, float* w_a, int* sel_e, float* sel_v) {
   constexpr int kPer = MIRA_MAX_EXPERTS / 64;  // experts per lane
   const int lane = threadIdx.x & 63;
+  if (E <= 64) {
+    // one expert per lane: the selection stays in registers (the same keys,
+    // exponentials and sum order as below, so the results are identical)
+    const bool in = lane < E;
+    const float v = in ? lgrow[lane] : 0.f;
+    const uint32_t key = f32_order_key(v);
+    int rank = 0;
+#pragma unroll 1
+    for (int l2 = 0; l2 < E; ++l2) {
+      const uint32_t k2 = (uint32_t)__builtin_amdgcn_readlane((int)key, l2);
+      rank += (k2 > key) || (k2 == key && l2 < lane);
+    }
+    const bool sel = in && rank < k;
+    const int l0 = __builtin_ctzll(__ballot(sel && rank == 0));
+    const float vmax = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l0));
+    const float ex = in ? expf(v - vmax) : 0.f;
+    float denom = 0.f;
+    if (softmax_all) {
+      denom = wave_sum(ex);
+    } else {
+#pragma unroll 1
+      for (int j = 0; j < k; ++j) {
+        const int lj = __builtin_ctzll(__ballot(sel && rank == j));
+        denom += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ex), lj));
+      }
+    }
+    if (sel) {
+      idx_a[rank] = lane;
+      w_a[rank] = ex / denom;
+    }
+    return;
+  }
   const int nblk = (E + 63) / 64;
   // each lane keeps the logits of experts lane, lane+64, ... in registers;
   // the comparison keys of the other experts come from v_readlane
@@ -385,6 +417,148 @@ __device__ inline void permute_decode_wave(const int32_t* idx, const float* wts,
     o.misc[MISC_MTOTAL] = 0;
     if (ep.status) *ep.status = bits;
   }
+}
+
+// ---------------------------------------------------------------------------
+// Stable grouping of a decode call with at most 64 routed pairs (one per
+// lane), in registers.  For the pair p of lane p with expert e: eq = the
+// pairs of the same expert and lo = the pairs of a lower expert, from one
+// ballot per bit of the expert index (most significant first).  Then the
+// pair's position is |lo| + (earlier pairs in eq), and its group's index
+// among the non-empty routed groups is the number of group leaders (first
+// pairs) in lo.  The order is the one permute_decode_wave produces.
+// ---------------------------------------------------------------------------
+constexpr int kDecodeSmallPairs = 64;
+
+__device__ __forceinline__ void pair_masks(bool ok, int e, int E, uint64_t& eq, uint64_t& lo) {
+  const int nbits = E > 1 ? 32 - __builtin_clz((unsigned)(E - 1)) : 0;
+  eq = __ballot(ok);
+  lo = 0;
+  for (int b = nbits - 1; b >= 0; --b) {
+    const bool bit = (e >> b) & 1;
+    const uint64_t ones = __ballot(ok && bit);
+    if (bit) lo |= eq & ~ones;
+    eq &= bit ? ones : ~ones;
+  }
+  if (!ok) eq = lo = 0;
+}
+
+__device__ __forceinline__ int wave_or(int v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v |= __shfl_xor(v, o, 64);
+  return v;
+}
+
+// DecodeWork descriptors and the residency status of a call with T*k <= 64
+// pairs (one wave): what the expert kernels read.  Positions i >= n of a
+// descriptor are left as they were (the kernels read only i < n).
+__device__ inline void decode_work_small(const int32_t* idx_s, const float* w_s, const int* xe_s,
+                                         const int* slot_s, int T, int k, int E, int S,
+                                         const ExpertPool& ep, DecodeWork* __restrict__ work,
+                                         int max_active) {
+  const int lane = threadIdx.x & 63;
+  const int P = T * k;
+  const bool ok = lane < P;
+  const int e = ok ? idx_s[lane] : 0;
+  const float w = ok ? w_s[lane] : 0.f;
+  uint64_t eq, lo;
+  pair_masks(ok, e, E, eq, lo);
+  const uint64_t lt = lane ? (~0ull >> (64 - lane)) : 0ull;
+  const int rank = __popcll(eq & lt);
+  const bool lead = ok && rank == 0;
+  const uint64_t leaders = __ballot(lead);
+  const int a = __popcll(lo & leaders), nr = __popcll(leaders);
+  int bits = 0;
+  if (lead) {
+    const int slot = slot_s[e];
+    bits |= slot < 0 ? 1 : (slot >= ep.n_slots ? 2 : 0);
+    DecodeWork* wk = work + a;
+    wk->group = e;
+    wk->slot = slot;
+    wk->off = __popcll(lo);
+    wk->n = __popcll(eq);
+  }
+  if (ok) {
+    const int t = lane / k;
+    DecodeWork* wk = work + a;
+    wk->tok[rank] = t;
+    wk->xe[rank] = xe_s[t];
+    wk->w[rank] = w;
+  }
+  // shared experts follow the routed groups: every token in order, weight 1
+  for (int s = lane; s < S; s += 64) {
+    const int slot = slot_s[E + s];
+    bits |= slot < 0 ? 1 : (slot >= ep.n_slots ? 2 : 0);
+    DecodeWork* wk = work + nr + s;
+    wk->group = E + s;
+    wk->slot = slot;
+    wk->off = P + s * T;
+    wk->n = T;
+  }
+  for (int i = lane; i < S * T; i += 64) {
+    const int s = i / T, t = i - s * T;
+    DecodeWork* wk = work + nr + s;
+    wk->tok[t] = t;
+    wk->xe[t] = xe_s[t];
+    wk->w[t] = 1.0f;
+  }
+  for (int aa = nr + S + lane; aa < max_active; aa += 64) work[aa].group = -1;
+  bits = wave_or(bits);
+  if (lane == 0 && ep.status) *ep.status = bits;
+}
+
+// The caller's optional routing outputs of a call with T*k <= 64 pairs (one
+// wave, beside decode_work_small): top-k, permutation order, group counts
+// and offsets.  cnt_s: LDS scratch of E ints.
+__device__ inline void decode_outputs_small(const int32_t* idx_s, const float* w_s, int T, int k,
+                                            int E, int S, const PermOut& o, int* cnt_s) {
+  const int lane = threadIdx.x & 63;
+  const int P = T * k, G = E + S;
+  const bool ok = lane < P;
+  const int e = ok ? idx_s[lane] : 0;
+  if (ok) {
+    if (o.idx_out) o.idx_out[lane] = e;
+    if (o.w_out) o.w_out[lane] = w_s[lane];
+  }
+  if (!o.order_out && !o.counts_out && !o.offsets_out) return;
+  uint64_t eq, lo;
+  pair_masks(ok, e, E, eq, lo);
+  const uint64_t lt = lane ? (~0ull >> (64 - lane)) : 0ull;
+  const int rank = __popcll(eq & lt);
+  if (o.order_out) {
+    if (ok) o.order_out[__popcll(lo) + rank] = lane;
+    for (int i = lane; i < S * T; i += 64) o.order_out[P + i] = P + i;
+  }
+  if (!o.counts_out && !o.offsets_out) return;
+  for (int g = lane; g < E; g += 64) cnt_s[g] = 0;
+  __builtin_amdgcn_wave_barrier();
+  if (ok && rank == 0) cnt_s[e] = __popcll(eq);
+  __builtin_amdgcn_wave_barrier();
+  // exclusive scan over groups, 4 consecutive groups per lane
+  int c4[4], sum = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int g = lane * 4 + i;
+    c4[i] = g < E ? cnt_s[g] : (g < G ? T : 0);
+    sum += c4[i];
+  }
+  int incl = sum;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int v = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += v;
+  }
+  int run = incl - sum;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int g = lane * 4 + i;
+    if (g < G) {
+      if (o.counts_out) o.counts_out[g] = c4[i];
+      if (o.offsets_out) o.offsets_out[g] = run;
+    }
+    run += c4[i];
+  }
+  if (lane == 63 && o.offsets_out) o.offsets_out[G] = incl;
 }
 
 inline PermOut perm_out(const WsPtr& w, int32_t* counts_out, int32_t* idx_out, float* wts_out,
