@@ -32,6 +32,7 @@ METRIC = "MoE-layer tokens/s (decode+prefill); HBM GB/s on packed experts vs pea
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 COLD_BYTES = 1 << 30
+PROF_EVERY = 8  # steps timed with events: one layer-copy rotation in every 8
 
 # HBM bytes per launch of the dominant kernels, from two rocprofv3 --pmc runs
 # (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch, averaged) on this bench's
@@ -654,27 +655,41 @@ def main():
 
     decode = T <= mira.MIRA_DECODE_MAX_TOKENS
     dominant = "decode_gateup" if decode else "prefill_gateup"
-    if not args.no_profile:
-        # only the dominant kernel carries event records (events cost time)
+    prof_on = not args.no_profile
+
+    def sampled(i):
+        # one rotation over the layer copies in every PROF_EVERY carries the
+        # events (each event pair adds a few microseconds to its step)
+        return prof_on and (i // len(argsets)) % PROF_EVERY == 0
+
+    if prof_on:
+        # only the dominant kernel carries event records
         mira.mira_profile_select(dominant)
-        mira.mira_profile_enable(True)
+        mira.mira_profile_enable(False)
         mira.mira_profile_read()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(i)
+        if sampled(i):
+            mira.mira_profile_enable(True)
+            step(i)
+            mira.mira_profile_enable(False)
+        else:
+            step(i)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     prof = {}
-    if not args.no_profile:
+    if prof_on:
         prof = mira.mira_profile_read()
-        mira.mira_profile_enable(False)
 
     ms = elapsed * 1e3 / args.steps
     value = T / (ms / 1e3)
-    # average algorithmic units per step over the rotation actually timed
+    # average algorithmic units per step over the rotation actually timed,
+    # and over the steps whose dominant launch carried the events
     n = args.steps
     avg = {k: sum(units[i % len(units)][k] for i in range(n)) / n for k in units[0]}
+    samp = [i for i in range(n) if sampled(i)] or [0]
+    avg_s = {k: sum(units[i % len(units)][k] for i in samp) / len(samp) for k in units[0]}
     roof = None
     if prof:
         if decode:
@@ -682,24 +697,26 @@ def main():
             cnt, tot = prof.get(name, (0, 0.0))
             if cnt:
                 dur = tot / cnt * 1e-3
-                achieved = avg["gu_bytes"] / dur / 1e9
+                achieved = avg_s["gu_bytes"] / dur / 1e9
                 roof = {"bound": "hbm", "kernel": name, "achieved": round(achieved, 1),
                         "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                         "traffic": traffic_bytes(name, cfg.name if fmt == "int8" else f"{cfg.name}_int4"),
                         "avg_us": round(dur * 1e6, 2),
-                        "algorithmic_bytes_per_launch": int(avg["gu_bytes"])}
+                        "algorithmic_bytes_per_launch": int(avg_s["gu_bytes"]),
+                        "timed_launches": cnt}
         else:
             name = "prefill_gateup"
             cnt, tot = prof.get(name, (0, 0.0))
             if cnt:
                 dur = tot / cnt * 1e-3
-                achieved = avg["gu_flops"] / dur / 1e12
+                achieved = avg_s["gu_flops"] / dur / 1e12
                 roof = {"bound": "mfma", "kernel": name, "achieved": round(achieved, 1),
                         "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                         "frac": round(achieved / BF16_PEAK_TFLOPS, 4),
                         "traffic": traffic_bytes(name, cfg.name),
                         "avg_us": round(dur * 1e6, 2),
-                        "algorithmic_flops_per_launch": avg["gu_flops"]}
+                        "algorithmic_flops_per_launch": avg_s["gu_flops"],
+                        "timed_launches": cnt}
     step_bytes = avg["gu_bytes"] + avg["dn_bytes"]
     line = {
         "metric": METRIC,
