@@ -72,6 +72,23 @@ def test_fine_grained_shape_small(mira, T):
     run_and_check(Layer(SMALL_FG, T=T))
 
 
+# The largest expert count the interface takes (E + S = MIRA_MAX_EXPERTS):
+# top-k over four 64-expert blocks per lane, 256 groups in the permutation
+# and the decode descriptors (one-wave path beyond 64 pairs), and 16 expert
+# tiles in the prefill router.  Decode routing equals prefill routing here too.
+LARGE_E = _cfg("large_e", 106, T=16, C=128, E=255, k=8, R=64, S=1, zipf_s=1.0)
+
+
+@pytest.mark.parametrize("T", [1, 9, 16, 40])
+def test_largest_expert_count(mira, T):
+    lay = Layer(LARGE_E, T=T)
+    res, _, _, _ = run_and_check(lay)
+    if T <= mira.MIRA_DECODE_MAX_TOKENS:
+        pre = lay.run(mira.MIRA_FLAG_FORCE_PREFILL)
+        for key in ("idx", "w", "logits", "counts", "offsets", "order"):
+            assert np.array_equal(res[key], pre[key]), key
+
+
 @pytest.mark.parametrize("flags", [0, "decode", "prefill"])
 def test_f32_activations_k_equals_E(mira, flags):
     f = {0: 0, "decode": mira.MIRA_FLAG_FORCE_DECODE, "prefill": mira.MIRA_FLAG_FORCE_PREFILL}[flags]
