@@ -59,6 +59,49 @@ __global__ __launch_bounds__(kBigThreads) void route_kernel(
 }
 
 
+// Prefill routing over several expert tiles (bf16, E > 16): one workgroup
+// per (16 tokens, tile of 16 experts), each tile summed exactly as above,
+// logits to the workspace; topk_kernel then selects.  The tiles of a token
+// group no longer run one after another in a single workgroup.
+__global__ __launch_bounds__(kBigThreads) void route_tile_kernel(
+    const uint16_t* __restrict__ x, const uint16_t* __restrict__ wr, const float* __restrict__ bias,
+    int T, int E, int C, float* __restrict__ logits_ws, float* __restrict__ logits_out) {
+  __shared__ float lg[kRouteTok][MIRA_MAX_EXPERTS];
+  __shared__ float part[kBigWaves][16][17];
+  __shared__ float bias_s[MIRA_MAX_EXPERTS];
+  const int tid = threadIdx.x;
+  const int t0 = blockIdx.x * kRouteTok, nt = min(kRouteTok, T - t0), et = blockIdx.y;
+  const int e_lo = et * 16, ne = min(16, E - e_lo);
+  const float b_r = (bias && tid < ne) ? bias[e_lo + tid] : 0.f;
+  auto stage = [&]() {
+    if (tid < ne) bias_s[e_lo + tid] = b_r;
+  };
+  logits_ksplit_bf16(x + (size_t)t0 * C, wr, bias ? bias_s : nullptr, nt, E, C, part, lg, nullptr,
+                     stage, et, et + 1);
+  if (tid < nt * 16) {
+    const int tt = tid >> 4, ee = tid & 15;
+    if (ee < ne) {
+      const size_t i = (size_t)(t0 + tt) * E + e_lo + ee;
+      logits_ws[i] = lg[tt][e_lo + ee];
+      if (logits_out) logits_out[i] = lg[tt][e_lo + ee];
+    }
+  }
+}
+
+// Top-k and combine weights from the workspace logits, one wave per token.
+__global__ __launch_bounds__(kBigThreads) void topk_kernel(const float* __restrict__ logits_ws,
+                                                           int T, int E, int k, int softmax_all,
+                                                           int32_t* __restrict__ idx_ws,
+                                                           float* __restrict__ w_ws) {
+  __shared__ int sel_e[kBigWaves][MIRA_MAX_TOPK];
+  __shared__ float sel_v[kBigWaves][MIRA_MAX_TOPK];
+  const int wave = threadIdx.x >> 6;
+  const int t = blockIdx.x * kBigWaves + wave;
+  if (t >= T) return;
+  topk_rank(logits_ws + (size_t)t * E, E, k, softmax_all, idx_ws + (size_t)t * k,
+            w_ws + (size_t)t * k, sel_e[wave], sel_v[wave]);
+}
+
 // Group counts and their exclusive scan (wave 0; each lane owns 4
 // consecutive groups): routed group g < E holds count(g) pairs, shared group
 // E + s holds T.  Writes off_s[0..G] in LDS and the counts outputs.
@@ -467,7 +510,13 @@ hipError_t launch_route(const mira_shape& s, const Layout& L, const WsPtr& w, co
   dim3 grid((T + kRouteTok - 1) / kRouteTok), block(kBigThreads);
   const int sa = (s.flags & MIRA_FLAG_SOFTMAX_ALL) ? 1 : 0;
   prof_begin("route", st);
-  if (s.act_dtype == MIRA_BF16)
+  const int n_et = (L.E + 15) / 16;
+  if (s.act_dtype == MIRA_BF16 && n_et > 1) {
+    hipLaunchKernelGGL(route_tile_kernel, dim3(grid.x, n_et), block, 0, st, (const uint16_t*)x,
+                       (const uint16_t*)wr, bias, T, L.E, L.C, w.logits, logits_out);
+    hipLaunchKernelGGL(topk_kernel, dim3((T + kBigWaves - 1) / kBigWaves), block, 0, st,
+                       (const float*)w.logits, T, L.E, L.k, sa, w.idx, w.wts);
+  } else if (s.act_dtype == MIRA_BF16)
     hipLaunchKernelGGL(route_kernel<uint16_t>, grid, block, 0, st, (const uint16_t*)x,
                        (const uint16_t*)wr, bias, T, L.E, L.C, L.k, sa, w.logits, logits_out,
                        w.idx, w.wts);

@@ -61,15 +61,18 @@ __device__ __forceinline__ float absmax_bf16x8(v4i v) {
 
 // x points at the first of T <= 16 tokens.  If xmax is not null it also
 // receives max |x[t][:]| of each token; bias_s is the router bias (or null),
-// staged into LDS by pre_sync() right before the first barrier.
+// staged into LDS by pre_sync() right before the first barrier.  Expert
+// tiles et_begin .. et_end-1 of 16 experts are computed (all by default);
+// a tile's sums do not depend on which other tiles the call computes.
 template <typename PreSync>
 __device__ void logits_ksplit_bf16(const uint16_t* __restrict__ x, const uint16_t* __restrict__ wr,
                                    const float* bias_s, int T, int E, int C,
                                    float (*part)[16][17], float (*lg)[MIRA_MAX_EXPERTS],
-                                   float* xmax, PreSync pre_sync) {
+                                   float* xmax, PreSync pre_sync, int et_begin = 0,
+                                   int et_end = -1) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, kg = lane >> 4;
-  const int n_et = (E + 15) / 16, nch = C / 32;
+  const int n_et = et_end < 0 ? (E + 15) / 16 : et_end, nch = C / 32;
   const bool tok_ok = r16 < T;
   const uint16_t* xrow = x + (size_t)(tok_ok ? r16 : 0) * C + kg * 8;
   constexpr int B = 8;  // chunks in flight per wave
@@ -87,8 +90,8 @@ __device__ void logits_ksplit_bf16(const uint16_t* __restrict__ x, const uint16_
       a[u] = (ch < nch && e_ok) ? ld16(wrow + ch * 32) : zero16();
     }
   };
-  if (one_batch) load_rows(0);
-  for (int et = 0; et < n_et; ++et) {
+  if (one_batch) load_rows(et_begin);
+  for (int et = et_begin; et < n_et; ++et) {
     v4f acc = {0.f, 0.f, 0.f, 0.f};
     float xm = 0.f;
     for (int ch0 = wave; ch0 < nch; ch0 += B * kBigWaves) {
@@ -111,13 +114,13 @@ __device__ void logits_ksplit_bf16(const uint16_t* __restrict__ x, const uint16_
 #pragma unroll
       for (int u = 0; u < B; ++u) {
         acc = mfma_bf16(a[u], b[u], acc);
-        if (et == 0) xm = fmaxf(xm, absmax_bf16x8(b[u]));
+        if (et == et_begin) xm = fmaxf(xm, absmax_bf16x8(b[u]));
       }
     }
     if (one_batch && et + 1 < n_et) load_rows(et + 1);
 #pragma unroll
     for (int i = 0; i < 4; ++i) part[wave][r16][kg * 4 + i] = acc[i];  // [token][expert]
-    if (et == 0) {
+    if (et == et_begin) {
       // this wave's max over its chunks of token r16: combine the 4 lane groups
       xm = fmaxf(xm, __shfl_xor(xm, 16, 64));
       xm = fmaxf(xm, __shfl_xor(xm, 32, 64));
@@ -125,7 +128,7 @@ __device__ void logits_ksplit_bf16(const uint16_t* __restrict__ x, const uint16_
       pre_sync();  // caller's LDS staging, issued before the loads above
     }
     lds_barrier();
-    if (et == 0 && xmax && tid < 16) {
+    if (et == et_begin && xmax && tid < 16) {
       float m = 0.f;
       for (int w = 0; w < kBigWaves; ++w) m = fmaxf(m, part[w][tid][16]);
       xmax[tid] = m;
