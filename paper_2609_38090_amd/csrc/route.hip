@@ -4,8 +4,10 @@
 // combined).
 //
 // Two launch shapes share the device functions below:
-//  - prefill: route_kernel (16 tokens per workgroup) then permute_kernel
-//    (one workgroup);
+//  - prefill: route_kernel (16 tokens per workgroup), or with more than 16
+//    experts route_tile_kernel (one workgroup per 16 tokens and expert tile)
+//    and topk_kernel; then the permutation (one workgroup, or count and
+//    scatter kernels over chunks of pairs);
 //  - decode (T <= MIRA_DECODE_MAX_TOKENS): one workgroup runs router, top-k,
 //    permutation and the fixed-point digits of x back to back, so the
 //    expert kernels start after a single small launch.
