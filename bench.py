@@ -37,18 +37,18 @@ PROF_EVERY = 8  # steps timed with events: one layer-copy rotation in every 8
 # HBM bytes per launch of the dominant kernels, from two rocprofv3 --pmc runs
 # (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch, averaged) on this bench's
 # workload, each scaled by what the same counter reads for a plain 1 GiB
-# device copy (bench.py --copy-bytes 1073741824 reads FETCH_SIZE 524300 KiB
+# device copy (bench.py --copy-bytes 1073741824 reads FETCH_SIZE 524302 KiB
 # and WRITE_SIZE 1048576 KiB: scale 2.0 and 1.0).  An entry holds only for
 # the kernel sources it was measured on (hash of the kernel file and the two
 # shared headers); otherwise the bench reports traffic as null.
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 TRAFFIC = {
     ("decode_gateup", "mixtral_decode"): dict(sources=("decode.hip", "decode_dev.h", "int4_format.h"),
-                                               sha="e6d1a726c71d3fa1", fetch_kib=114817.3, write_kib=98.0),
+                                               sha="f897eff224f6afd6", fetch_kib=114817.3, write_kib=98.0),
     ("decode_gateup", "mixtral_decode_int4"): dict(sources=("decode.hip", "decode_dev.h", "int4_format.h"),
-                                                    sha="e6d1a726c71d3fa1", fetch_kib=61050.9, write_kib=98.0),
-    ("prefill_gateup", "mixtral_prefill"): dict(sources=("prefill.hip",), sha="e127507f028c6924",
-                                                 fetch_kib=602308.2, write_kib=38289.3),
+                                                    sha="f897eff224f6afd6", fetch_kib=61050.8, write_kib=98.0),
+    ("prefill_gateup", "mixtral_prefill"): dict(sources=("prefill.hip",), sha="d36f59a2f3ec2d7a",
+                                                 fetch_kib=601701.1, write_kib=38364.3),
 }
 
 
