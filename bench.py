@@ -168,6 +168,13 @@ def scale_bench(reps=200):
     return line
 
 
+def event_step(i, n_copies):
+    """Whether timed step i carries the dominant kernel's events: one rotation
+    over the layer copies in every PROF_EVERY (each event pair adds a few
+    microseconds to its step), so every copy is sampled equally often."""
+    return (i // n_copies) % PROF_EVERY == 0
+
+
 def expert_stride(cfg, fmt):
     import paper_2609_38090_amd as mira
     return (mira.mira_packed_expert_bytes_int4(cfg.C, cfg.R) if fmt == "int4"
@@ -211,8 +218,8 @@ def build_copies(cfg, n_copies, fmt="int8"):
 def algorithmic_units(cfg, counts, fmt="int8"):
     """Packed-expert bytes and FLOPs one call must touch, from the routed counts.
     INT8: gate and up (2RC) plus the shared scales (2R bytes) for gate/up, RC
-    for down; INT4: the 544-byte tiles (nibbles and their fp16 scales) of
-    gate and up, then of down."""
+    for down; INT4: per 16 rows x 64 columns, 512 bytes of nibbles and 32 of
+    fp16 scales (544 bytes), for gate and up, then for down."""
     active = [g for g in range(cfg.G) if counts[g] > 0]
     pairs = int(sum(counts))
     if fmt == "int4":
@@ -658,9 +665,7 @@ def main():
     prof_on = not args.no_profile
 
     def sampled(i):
-        # one rotation over the layer copies in every PROF_EVERY carries the
-        # events (each event pair adds a few microseconds to its step)
-        return prof_on and (i // len(argsets)) % PROF_EVERY == 0
+        return prof_on and event_step(i, len(argsets))
 
     if prof_on:
         # only the dominant kernel carries event records
