@@ -63,8 +63,8 @@ __global__ __launch_bounds__(kBigThreads) void route_kernel(
 
 // Prefill routing over several expert tiles (bf16, E > 16): one workgroup
 // per (16 tokens, tile of 16 experts), each tile summed exactly as above,
-// logits to the workspace; topk_kernel then selects.  The tiles of a token
-// group no longer run one after another in a single workgroup.
+// logits to the workspace; topk_kernel then selects.  So the tiles of a
+// token group run side by side on different CUs.
 __global__ __launch_bounds__(kBigThreads) void route_tile_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ wr, const float* __restrict__ bias,
     int T, int E, int C, float* __restrict__ logits_ws, float* __restrict__ logits_out) {
