@@ -21,7 +21,7 @@ namespace mira {
 template <typename ActT>
 __global__ __launch_bounds__(kBigThreads) void route_kernel(
     const ActT* __restrict__ x, const ActT* __restrict__ wr, const float* __restrict__ bias,
-    int T, int E, int C, int k, int softmax_all, float* __restrict__ logits_ws,
+    int T, int E, int C, int k, int softmax_all, int tpw, float* __restrict__ logits_ws,
     float* __restrict__ logits_out, int32_t* __restrict__ idx_ws, float* __restrict__ w_ws) {
   __shared__ float lg[kRouteTok][MIRA_MAX_EXPERTS];
   __shared__ float part[kBigWaves][16][17];
@@ -29,7 +29,7 @@ __global__ __launch_bounds__(kBigThreads) void route_kernel(
   __shared__ int sel_e[kBigWaves][MIRA_MAX_TOPK];
   __shared__ float sel_v[kBigWaves][MIRA_MAX_TOPK];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int t0 = blockIdx.x * kRouteTok, nt = min(kRouteTok, T - t0);
+  const int t0 = blockIdx.x * tpw, nt = min(tpw, T - t0);  // tpw tokens per workgroup
   float bias_r[MIRA_MAX_EXPERTS / kBigThreads + 1];
 #pragma unroll
   for (int i = 0; i <= MIRA_MAX_EXPERTS / kBigThreads; ++i) {
@@ -67,12 +67,12 @@ __global__ __launch_bounds__(kBigThreads) void route_kernel(
 // token group run side by side on different CUs.
 __global__ __launch_bounds__(kBigThreads) void route_tile_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ wr, const float* __restrict__ bias,
-    int T, int E, int C, float* __restrict__ logits_ws, float* __restrict__ logits_out) {
+    int T, int E, int C, int tpw, float* __restrict__ logits_ws, float* __restrict__ logits_out) {
   __shared__ float lg[kRouteTok][MIRA_MAX_EXPERTS];
   __shared__ float part[kBigWaves][16][17];
   __shared__ float bias_s[MIRA_MAX_EXPERTS];
   const int tid = threadIdx.x;
-  const int t0 = blockIdx.x * kRouteTok, nt = min(kRouteTok, T - t0), et = blockIdx.y;
+  const int t0 = blockIdx.x * tpw, nt = min(tpw, T - t0), et = blockIdx.y;
   const int e_lo = et * 16, ne = min(16, E - e_lo);
   const float b_r = (bias && tid < ne) ? bias[e_lo + tid] : 0.f;
   auto stage = [&]() {
@@ -509,23 +509,28 @@ hipError_t launch_route(const mira_shape& s, const Layout& L, const WsPtr& w, co
                         const void* wr, const float* bias, float* logits_out, hipStream_t st) {
   const int T = L.T;
   if (T == 0) return hipSuccess;
-  dim3 grid((T + kRouteTok - 1) / kRouteTok), block(kBigThreads);
+  // bf16 with one expert tile: a few tokens per workgroup, so the 16 router
+  // rows (read by every workgroup) stream into many CUs at once; a token's
+  // sums do not depend on which other tokens share its MFMA operand.  With
+  // several tiles, more workgroups would re-read every tile's rows.
+  const int n_et = (L.E + 15) / 16;
+  const int tpw = (s.act_dtype == MIRA_BF16 && n_et == 1) ? kRouteTokBf16 : kRouteTok;
+  dim3 grid((T + tpw - 1) / tpw), block(kBigThreads);
   const int sa = (s.flags & MIRA_FLAG_SOFTMAX_ALL) ? 1 : 0;
   prof_begin("route", st);
-  const int n_et = (L.E + 15) / 16;
   if (s.act_dtype == MIRA_BF16 && n_et > 1) {
     hipLaunchKernelGGL(route_tile_kernel, dim3(grid.x, n_et), block, 0, st, (const uint16_t*)x,
-                       (const uint16_t*)wr, bias, T, L.E, L.C, w.logits, logits_out);
+                       (const uint16_t*)wr, bias, T, L.E, L.C, tpw, w.logits, logits_out);
     hipLaunchKernelGGL(topk_kernel, dim3((T + kBigWaves - 1) / kBigWaves), block, 0, st,
                        (const float*)w.logits, T, L.E, L.k, sa, w.idx, w.wts);
   } else if (s.act_dtype == MIRA_BF16)
     hipLaunchKernelGGL(route_kernel<uint16_t>, grid, block, 0, st, (const uint16_t*)x,
-                       (const uint16_t*)wr, bias, T, L.E, L.C, L.k, sa, w.logits, logits_out,
+                       (const uint16_t*)wr, bias, T, L.E, L.C, L.k, sa, tpw, w.logits, logits_out,
                        w.idx, w.wts);
   else
     hipLaunchKernelGGL(route_kernel<float>, grid, block, 0, st, (const float*)x,
-                       (const float*)wr, bias, T, L.E, L.C, L.k, sa, w.logits, logits_out, w.idx,
-                       w.wts);
+                       (const float*)wr, bias, T, L.E, L.C, L.k, sa, tpw, w.logits, logits_out,
+                       w.idx, w.wts);
   prof_end("route", st);
   return hipGetLastError();
 }

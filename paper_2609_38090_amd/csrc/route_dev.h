@@ -9,7 +9,8 @@
 
 namespace mira {
 
-constexpr int kRouteTok = 16;  // tokens per route workgroup
+constexpr int kRouteTok = 16;  // tokens per route workgroup (at most)
+constexpr int kRouteTokBf16 = 4;  // tokens per prefill route workgroup, bf16, one expert tile
 constexpr int kBigThreads = 1024;  // permutation and decode-prep workgroups
 static_assert(kPermChunk == kBigThreads, "the chunked permutation runs one thread per pair");
 constexpr int kBigWaves = kBigThreads / 64;
