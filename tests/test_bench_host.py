@@ -51,12 +51,21 @@ def test_prefill_flops_count_every_pair():
 
 
 def test_traffic_entries_follow_the_sources(monkeypatch):
+    # an entry counts only while the kernel sources hash to the value it was
+    # measured on; then it is the scaled counter bytes per launch
     for key, ent in bench.TRAFFIC.items():
+        monkeypatch.setattr(bench, "source_hash", lambda sources, sha=ent["sha"]: sha)
         got = bench.traffic_bytes(*key)
         assert got == int((ent["fetch_kib"] * bench.FETCH_SCALE + ent["write_kib"] * bench.WRITE_SCALE) * 1024)
     monkeypatch.setattr(bench, "source_hash", lambda sources: "0" * 16)
     assert all(bench.traffic_bytes(*key) is None for key in bench.TRAFFIC)
     assert bench.traffic_bytes("decode_gateup", "no_such_workload") is None
+
+
+def test_source_hash_covers_the_shared_headers(tmp_path, monkeypatch):
+    h = bench.source_hash(("decode.hip",))
+    assert len(h) == 16 and h == bench.source_hash(("decode.hip",))
+    assert h != bench.source_hash(("prefill.hip",))
 
 
 @pytest.mark.parametrize("steps,copies", [(200, 5), (200, 2), (100, 3), (7, 4)])
