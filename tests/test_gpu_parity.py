@@ -89,6 +89,28 @@ def test_largest_expert_count(mira, T):
             assert np.array_equal(res[key], pre[key]), key
 
 
+@pytest.mark.parametrize("T", [3, 24])
+def test_softmax_over_all_experts_large_e(mira, T):
+    # the selection over four 64-expert blocks per lane with the weights of a
+    # softmax over all 255 experts: against the GPU's own exported logits
+    # (exhaustive sort, fp64 softmax), so near ties cannot matter
+    c = LARGE_E
+    lay = Layer(c, T=T)
+    res = lay.run(mira.MIRA_FLAG_SOFTMAX_ALL)
+    assert res["status"][0] == 0
+    for t in range(T):
+        row = res["logits"][t].astype(np.float64)
+        brute = sorted(range(c.E), key=lambda e: (-float(res["logits"][t, e]), e))[:c.k]
+        assert res["idx"][t].tolist() == brute, t
+        p = np.exp(row - row.max())
+        p /= p.sum()
+        assert np.max(np.abs(res["w"][t] - p[brute])) < 2e-6, t
+    if T <= mira.MIRA_DECODE_MAX_TOKENS:
+        pre = lay.run(mira.MIRA_FLAG_SOFTMAX_ALL | mira.MIRA_FLAG_FORCE_PREFILL)
+        for key in ("idx", "w", "logits", "counts", "offsets", "order"):
+            assert np.array_equal(res[key], pre[key]), key
+
+
 @pytest.mark.parametrize("flags", [0, "decode", "prefill"])
 def test_f32_activations_k_equals_E(mira, flags):
     f = {0: 0, "decode": mira.MIRA_FLAG_FORCE_DECODE, "prefill": mira.MIRA_FLAG_FORCE_PREFILL}[flags]
