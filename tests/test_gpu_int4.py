@@ -49,6 +49,7 @@ def test_device_pack_int4_bf16_input_and_padding(mira):
 
 @pytest.mark.parametrize("cfg,T", [(CONFIGS["tiny"], 16), (SMALL_BF16, 1), (SMALL_BF16, 3), (SMALL_BF16, 5),
                                    (SMALL_BF16, 8), (SMALL_BF16, 16), (SMALL_FG, 1), (SMALL_FG, 2),
+                                   (SMALL_FG, 16),
                                    (SMALL_F32, 5), (SMALL_F32, 11), (WIDE, 1), (WIDE, 4), (WIDE, 9),
                                    (TALL, 2), (TALL, 7)])
 def test_int4_decode_matches_oracle(mira, cfg, T):
@@ -65,6 +66,18 @@ def test_int4_two_phase_and_repeat_bit_identical(mira):
     for key in a:
         assert np.array_equal(a[key], b[key]), key
         assert np.array_equal(a[key], c[key]), key
+
+
+def test_int4_non_resident_expert_sets_status(mira):
+    # the LDS-digit gate/up kernel returns before its barrier for a missing
+    # expert; the other experts' outputs are still written
+    lay = Layer(SMALL_BF16, T=5, fmt="int4", resident=[1, 2, 3, 4, 5, 6, 7])
+    res = lay.run()
+    assert res["counts"][0] > 0 and res["status"][0] & 1
+    assert np.all(np.isfinite(res["out"]))
+    lay2 = Layer(SMALL_BF16, T=1, fmt="int4")
+    lay2.table[int(lay2.run()["idx"][0, 0])] = 99   # beyond n_slots: skipped, flagged
+    assert lay2.run()["status"][0] & 2
 
 
 def test_int4_rejects_prefill(mira):
