@@ -91,7 +91,9 @@ class Layer:
         c = self.cfg
         return mira.MoEShape(c.C, c.R, c.E, c.k, c.S, act_dtype(c), flags | self.fflag)
 
-    def run(self, flags=0, two_phase=False, between=None):
+    def run(self, flags=0, two_phase=False, between=None, stream=None, sync=True):
+        """One layer call; returns the outputs as numpy arrays, or with
+        sync=False the device tensors (the call only queued on stream)."""
         c, T, dev = self.cfg, self.T, self.device
         s = self.shape(flags)
         P = T * c.k + c.S * T
@@ -113,12 +115,15 @@ class Layer:
                          expert_offsets=r["offsets"], pair_order=r["order"], workspace=ws,
                          workspace_bytes=ws.numel())
         if two_phase:
-            mira.mira_moe_route(s, a)
+            mira.mira_moe_route(s, a, stream)
             if between is not None:
                 between(r)
-            mira.mira_moe_experts(s, a)
+            mira.mira_moe_experts(s, a, stream)
         else:
-            mira.mira_moe_forward(s, a)
+            mira.mira_moe_forward(s, a, stream)
+        if not sync:
+            r["_ws"] = ws  # keep the workspace alive until the caller synchronizes
+            return r
         torch.cuda.synchronize()
         return {k: v.cpu().numpy() for k, v in r.items()}
 
