@@ -27,6 +27,10 @@
  *    valid once the stream reaches the call.  Only the host path of
  *    mira_pack_experts runs synchronously.  Calls on distinct workspaces may
  *    run concurrently.
+ *  - mira_moe_forward, mira_moe_route and mira_moe_experts only launch
+ *    kernels (no allocation, copy, memset or host synchronisation), so they
+ *    can be captured into a HIP graph and replayed; a replay recomputes
+ *    everything from the buffers the captured call was given.
  *  - Tensors are dense and row-major; shapes are given in brackets.
  */
 #ifndef MIRA_H_
