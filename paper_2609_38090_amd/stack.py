@@ -22,8 +22,10 @@ window.  Policy, per layer l of a step:
      go to the layer's telemetry;
   3. run the experts of layer l;
   4. prefetch controller: choose experts of layer l+2 (mode "predict": the
-     `stage_per_layer` best-scored experts of the predictor head; "oracle":
-     every expert layer l+2 will select, an upper bound; "demand": none); an
+     `stage_per_layer` best-scored experts of the predictor head; "oracle"
+     (oracle prefetch, a perfect predictor): every expert layer l+2 will
+     select, taken from that layer's routing as this library computed it on
+     an earlier pass, an upper bound; "demand": none); an
      expert already in HOT or STAGE is a skipped prefetch, a repeated request
      for the same (expert, layer) issues no second copy, and when no STAGE slot
      is free the prefetch is declined;
@@ -269,7 +271,8 @@ class ExpertStack:
     def step(self, mode: str = "predict", stage_per_layer: int = 2, true_idx=None,
              on_layer=None) -> StepStats:
         """One decode step through every layer.  true_idx[l] (the routing of
-        layer l) is needed by mode "oracle"; on_layer(l, out), if given, is
+        layer l, from an earlier pass of this stack) is needed by mode
+        "oracle"; on_layer(l, out), if given, is
         called after layer l's experts are queued (out is reused by the next
         layer, so copy it on the compute stream)."""
         st = StepStats()
