@@ -164,7 +164,9 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
 #pragma unroll
       for (int i = 0; i < 4; ++i) facc[cg][i] = 0.f;
 
-    constexpr int kDecUnroll = dec_unroll(NG);
+    // k-steps per batch: with 16 waves (four per SIMD, at most 128 registers
+    // each) half the batch of the 8-wave layout
+    constexpr int kDecUnroll = dec_unroll(NG) * 8 / KS;
     static_assert(kDecUnroll % 2 == 0 && kDecUnroll <= 16, "INT4 batches cover whole tiles");
     struct Batch {
       v4i a[I4 ? kDecUnroll / 2 : kDecUnroll], b[kDecUnroll][NG];
@@ -247,7 +249,9 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
   }
 }
 
-constexpr int kDownKS = 8;
+// 16 waves per workgroup: twice the loads in flight per CU of 8 waves with
+// batches of half the size (INT4 down 20.5 -> 18.0 us, INT8 unchanged)
+constexpr int kDownKS = 16;
 
 template <int NG, bool I4>
 static void launch_decode_down_ng(const Layout& L, const WsPtr& w, const ExpertPool& ep,
