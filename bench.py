@@ -44,9 +44,9 @@ PROF_EVERY = 8  # steps timed with events: one layer-copy rotation in every 8
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 TRAFFIC = {
     ("decode_gateup", "mixtral_decode"): dict(sources=("decode.hip", "decode_dev.h", "int4_format.h"),
-                                               sha="f897eff224f6afd6", fetch_kib=114817.3, write_kib=98.0),
+                                               sha="138b8c3d2a45bbb9", fetch_kib=114823.3, write_kib=98.0),
     ("decode_gateup", "mixtral_decode_int4"): dict(sources=("decode.hip", "decode_dev.h", "int4_format.h"),
-                                                    sha="f897eff224f6afd6", fetch_kib=61050.8, write_kib=98.0),
+                                                    sha="138b8c3d2a45bbb9", fetch_kib=61050.7, write_kib=98.0),
     ("prefill_gateup", "mixtral_prefill"): dict(sources=("prefill.hip",), sha="d36f59a2f3ec2d7a",
                                                  fetch_kib=601701.1, write_kib=38364.3),
 }
