@@ -112,20 +112,30 @@ size_t mira_packed_expert_bytes(int32_t hidden, int32_t ffn);
 
 /* ---- INT4 variant of the packed expert (MIRA_FLAG_INT4) -----------------
  * The 4-bit, group-64, fp16-scale format (the paper keeps INT8, section IV-B,
- * and lists INT4 as a quality point, Table I).  Per matrix [rows][K]
- * (gate [R][C], up [R][C], down [C][R], each with its own scales) and per row
- * and group of 64 consecutive columns:
+ * and lists INT4 as a quality point, Table I).  hidden and ffn must be
+ * multiples of 128.  Per matrix [rows][K] (gate [R][C], up [R][C], down
+ * [C][R], each with its own scales) and per row and group of 64 consecutive
+ * columns:
  *   alpha = max |w| over the group (exact),
  *   s     = fp16 of fl32(max(alpha, eps) / 7), round to nearest even; 2^-24
  *           if that rounds to zero, 65504 if it overflows,
  *   q     = clamp(rint_even(fl32(w / s)), -7, 7),  the weight is s * q.
- * Each matrix is stored as 16 x 64 tiles (tile-rows in order, column blocks
- * in order) of 544 bytes: 512 bytes of nibbles, then the 16 little-endian
- * fp16 scales of the tile's rows for its column block.  Inside a tile, the
- * 8-byte run g*16 + i holds row i, columns 16g .. 16g+15: byte b (0..7)
- * carries column 16g + 8*(b/4) + b%4 in its high nibble and that column + 4
- * in its low nibble, each as the two's complement of q.  gate, up and down
- * follow each other, zero-padded to a multiple of 256 bytes. */
+ * A matrix occupies M(rows, K) = rows*K/2 + rows*(K/64)*2 bytes: a nibble
+ * region of rows*K/2 bytes, then a scale region.
+ * Nibbles: tiles of 16 rows x 128 columns (two groups) of 1024 bytes, tile-rows
+ * in order and column pairs in order inside a tile-row.  Element (r, k) is in
+ * the byte at
+ *   ((r/16)*(K/128) + k/128)*1024 + ((k%64)/16*16 + r%16)*16
+ *     + ((k/64)%2)*8 + ((k%16)/8)*4 + k%4,
+ * in its high nibble if k%8 < 4 and in its low nibble otherwise, as the 4-bit
+ * two's complement of q.  (So the 16-byte run g*16 + i of a tile holds row i,
+ * columns 16g .. 16g+15 of the tile's first group in bytes 0..7 and of its
+ * second group in bytes 8..15.)
+ * Scales: the little-endian fp16 scale of row r and group k/64 is at
+ *   rows*K/2 + ((r/16)*(K/64) + k/64)*32 + (r%16)*2
+ * from the start of the matrix (by tile-row, then group, then the 16 rows).
+ * The blob holds gate at offset 0, up at M(R, C) and down at 2*M(R, C), then
+ * zero padding to a multiple of 256 bytes. */
 size_t mira_packed_expert_bytes_int4(int32_t hidden, int32_t ffn);
 
 /* Shape of one MoE layer. */
@@ -191,7 +201,12 @@ typedef struct mira_moe_args {
   uint64_t workspace_bytes;
 } mira_moe_args;
 
-/* Workspace needed by calls with up to max_tokens tokens (both paths). */
+/* Bytes of workspace needed by calls with up to max_tokens tokens (both
+ * paths): the pre-allocated working buffers of the expert step (section
+ * IV-F allocates its working buffers once, outside the per-layer path).  They
+ * hold the router logits, the routing and permutation, the activations'
+ * operand forms and the intermediate H' and expert outputs; nothing in them
+ * outlives a call.  Returns 0 for an invalid shape or a negative max_tokens. */
 size_t mira_workspace_bytes(const mira_shape* s, int32_t max_tokens);
 
 /* One MoE layer (section II-A; expert step of sections IV-A, IV-F):

@@ -4,16 +4,17 @@
 //   gate/up:  H'[pos][r] = sigma_r * silu(sigma_r * (Qg x)_r) * sigma_r * (Qu x)_r   (bf16)
 //   down:     Y[s][pos][c] = sum over the s-th k-chunk of r of Qd[c][r] * H'[pos][r]   (fp32)
 //   combine:  out[t] = sum_j w[t,j] * sum_s Y[s][inv[t*k+j]] + shared experts
-// A workgroup owns a tile of 256 weight rows (gate/up: 128 of each) by 128
+// A workgroup owns a tile of 512 weight rows (gate/up: 256 of each) by 128
 // tokens; its 4 waves split the weight rows, so every wave covers the same
 // tokens and all of them skip the 16-token subtiles past the group's end.
-// Packed int8 tiles go to LDS as they are (two stages, loads two stages
-// ahead) and each wave widens its own 16x32 operand fragments to bf16
+// Packed int8 tiles go to LDS as they are (a ring of three stages, loads two
+// stages ahead) and each wave widens its own 16x32 operand fragments to bf16
 // (exact: |q| <= 127) right before v_mfma_f32_16x16x32_bf16, which
 // accumulates in fp32.  Tiles (group, n-tile, k-chunk, m-tile) are walked by
 // a persistent grid whose tile count is read from the device, so the host
 // never waits for the routing; consecutive tiles share weights and land on
 // the same XCD (its L2).
+#include <mutex>
 #include <type_traits>
 
 #include "device_util.h"
@@ -896,7 +897,18 @@ __global__ __launch_bounds__(kGemmThreads) void prefill_gemm_kernel(
     }
     // the next tile's token rows load while this tile computes
     if (tau + nb < total) src_rows(describe(tau + nb), rows);
-    if (!ok) continue;
+    if (!ok) {
+      // A missing expert contributes nothing: its partial outputs are zero,
+      // so the combine (which sums every position's partials) leaves its term
+      // out.  Its H' rows stay unwritten; only this GEMM would read them.
+      if (!DUAL) {
+        float* yb = yout + (size_t)t.split * ysplit;
+        const int q4 = min(kTileRows, N - n0) / 4;
+        for (int i = tid; i < nv * q4; i += kGemmThreads)
+          *(v4f*)(yb + (size_t)(p0 + i / q4) * C + n0 + (i % q4) * 4) = v4f{0.f, 0.f, 0.f, 0.f};
+      }
+      continue;
+    }
 
     const int8_t* wstage0 = wbase + (size_t)ks0 * 1024;
     const int8_t* xstage0 = (const int8_t*)(act + (size_t)ks0 * 64);
@@ -964,16 +976,21 @@ __global__ __launch_bounds__(256) void f32_to_bf16_kernel(const float* __restric
     y[i] = f32_to_bf16_rne(x[i]);
 }
 
+// Workgroups of kernel k that fit on one CU, queried once per process (the
+// first caller fills the cache; concurrent callers wait for it).
 template <typename Kern>
-static int persistent_grid(Kern k, int& occ_cache, long max_tiles) {
-  if (occ_cache <= 0) {
-    int occ = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, k, kGemmThreads, 0) != hipSuccess ||
-        occ < 1)
-      occ = 1;
-    occ_cache = occ;
-  }
-  long cap = (long)device_cu_count() * occ_cache;
+static int gemm_occupancy(Kern k, std::once_flag& once, int& occ) {
+  std::call_once(once, [&] {
+    int o = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, k, kGemmThreads, 0) != hipSuccess || o < 1)
+      o = 1;
+    occ = o;
+  });
+  return occ;
+}
+
+static int persistent_grid(int occ, long max_tiles) {
+  long cap = (long)device_cu_count() * occ;
   if (max_tiles < cap) cap = max_tiles < 8 ? max_tiles : max_tiles / 8 * 8;
   return (int)(cap < 1 ? 1 : cap);
 }
@@ -993,17 +1010,19 @@ hipError_t launch_prefill(const mira_shape& s, const Layout& L, const WsPtr& w, 
   const size_t ysplit = (size_t)L.P * L.C;
   {
     auto kern = prefill_gemm_kernel<true>;
+    static std::once_flag once;
     static int occ = 0;
     const long tiles = (long)L.mt_max * ((L.R + kTileRows / 2 - 1) / (kTileRows / 2));
-    const int grid = persistent_grid(kern, occ, tiles);
+    const int grid = persistent_grid(gemm_occupancy(kern, once, occ), tiles);
     launch_timed("prefill_gateup", kern, dim3(grid), dim3(kGemmThreads), 0, st, L.C, L.R, L.G, 1,
                  ep, w.misc, w.offsets, w.tokpos, xb, w.hbuf, (float*)nullptr, (size_t)0);
   }
   {
     auto kern = prefill_gemm_kernel<false>;
+    static std::once_flag once;
     static int occ = 0;
     const long tiles = (long)L.mt_max * ((L.C + kTileRows - 1) / kTileRows) * L.ksplit;
-    const int grid = persistent_grid(kern, occ, tiles);
+    const int grid = persistent_grid(gemm_occupancy(kern, once, occ), tiles);
     launch_timed("prefill_down", kern, dim3(grid), dim3(kGemmThreads), 0, st, L.C, L.R, L.G,
                  L.ksplit, ep, w.misc, w.offsets, w.tokpos, (const uint16_t*)w.hbuf,
                  (uint16_t*)nullptr, w.ybuf, ysplit);

@@ -238,3 +238,19 @@ def test_int4_forward_argument_checks():
             _host_pack_i4(hidden, ffn, *(np.zeros((1, *sh_), dtype=np.float32)
                                          for sh_ in ((ffn, hidden), (ffn, hidden), (hidden, ffn))),
                           stride=256 * 1024)
+
+
+def test_host_pack_int4_matches_header_formulas():
+    """The library's host packer, read back through the header's INT4 offset
+    formulas (not through the oracle), stores the intended integers and
+    scales."""
+    import int4_layout as hl
+    C, R = 256, 128
+    (wg, wu, wd), q, sc = hl.marked_weights(C, R)
+    stride = mira.mira_packed_expert_bytes_int4(C, R)
+    out = np.zeros(stride, dtype=np.uint8)
+    mira.mira_pack_experts(mira.MoEShape(C, R, 1, 1, flags=mira.MIRA_FLAG_INT4), 1, mira.MIRA_F32,
+                           wg.ctypes.data, wu.ctypes.data, wd.ctypes.data, 1e-8, out.ctypes.data, stride, 0)
+    for (gq, gs), name in zip(hl.decode_blob(out, C, R), ("gate", "up", "down")):
+        assert np.array_equal(gq, q[name]), name
+        assert np.array_equal(gs.astype(np.float64), sc[name]), name

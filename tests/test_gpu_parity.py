@@ -158,6 +158,59 @@ def test_non_resident_selected_expert_sets_status(mira):
     assert res2["status"][0] & 2
 
 
+class _ZeroExpert:
+    """Oracle blobs with one expert replaced by an all-zero blob (sigma = 0,
+    q = 0), whose FFN output is exactly zero: the oracle's layer output with
+    that expert's term left out and every other term and weight unchanged."""
+
+    def __init__(self, blobs, missing, nbytes):
+        self.blobs, self.missing, self.nbytes = blobs, missing, nbytes
+
+    def __len__(self):
+        return len(self.blobs)
+
+    def __getitem__(self, e):
+        return np.zeros(self.nbytes, dtype=np.uint8) if e == self.missing else self.blobs[e]
+
+
+@pytest.mark.parametrize("T,path", [(16, "decode"), (16, "prefill"), (150, "prefill"), (150, "auto")])
+def test_missing_selected_expert_contributes_nothing(mira, T, path):
+    """A selected expert whose slot is -1 sets status bit 0 and its term is
+    missing from out (every other term present), on both expert paths.  The
+    workspace starts as NaN bytes, so a combine that read the missing
+    expert's never-written rows would show."""
+    from gpu_layer import LazyBlobs, check_routing
+    flags = {"decode": mira.MIRA_FLAG_FORCE_DECODE, "prefill": mira.MIRA_FLAG_FORCE_PREFILL,
+             "auto": 0}[path]
+    cfg = SMALL_BF16
+    lay = Layer(cfg, T=T, resident=[1, 2, 3, 4, 5, 6, 7])
+    res = lay.run(flags, ws_fill=0xFF)
+    assert res["counts"][0] > 0
+    assert res["status"][0] == 1
+    o_x, o_wr, o_b = lay.oracle_inputs()
+    o_logits = oracle.router_logits(o_x, o_wr, o_b)
+    assert not check_routing(res, lay, o_logits)  # no near ties at this seed
+    blobs = _ZeroExpert(LazyBlobs(lay), 0, lay.stride)
+    ref = oracle.moe_forward(o_x, o_wr, o_b, blobs, cfg.k, cfg.C, cfg.R)["out"]
+    assert_ffn_close(res["out"], ref, f"missing expert 0, {path}")
+
+
+# The down GEMM of the prefill path splits its contraction R into KS chunks
+# (KS <= R/4096, at most 4) and the combine sums the chunk partials in order.
+# With C = 256 the layer has one 512-row output tile, so at 300 tokens over
+# 4 experts (at most 8 m-tiles of 128) the grid's cost rule picks the largest
+# split: KS = 2 at R = 8192 and KS = 4 at R = 16384.  Every row is checked.
+KSPLIT_R8K = _cfg("ksplit_r8k", 107, T=300, C=256, E=4, k=2, R=8192, zipf_s=1.2)
+KSPLIT_R16K = _cfg("ksplit_r16k", 108, T=300, C=256, E=4, k=2, R=16384, zipf_s=1.2)
+
+
+@pytest.mark.parametrize("cfg", [KSPLIT_R8K, KSPLIT_R16K], ids=lambda c: c.name)
+def test_prefill_down_k_split_all_rows(mira, cfg):
+    lay = Layer(cfg)
+    res, errs, _, _ = run_and_check(lay, flags=mira.MIRA_FLAG_FORCE_PREFILL)
+    print(f"{cfg.name}: rel_fro={errs[0]:.2e} max_abs/rms={errs[1]:.2e}")
+
+
 def test_two_phase_demand_fetch_through_pinned_store(mira):
     """Route, read the counts, stage the missing experts from pinned host
     memory into spare slots, then run the experts: bit-identical to the

@@ -137,3 +137,19 @@ def test_int4_ffn_uses_the_dequantized_weights():
     assert np.allclose(oracle.expert_ffn(blob, x, C, R, "int4"), y, rtol=1e-12, atol=1e-15)
     with pytest.raises(ValueError):
         oracle.expert_ffn(blob, x, C, R, "int3")
+
+
+def test_layout_matches_header_formulas_everywhere():
+    """Every nibble and scale of an INT4 blob, read back through the header's
+    offset formulas, gives the integers and scales the weights were made
+    from; the marks differ pairwise in every part of the address, so a
+    swapped or misplaced axis of the layout fails."""
+    import int4_layout as hl
+    C, R = 256, 128
+    w, q, sc = hl.marked_weights(C, R)
+    blob = oracle.pack_expert_int4(*w)
+    assert blob.size == oracle.packed_expert_bytes_int4(C, R)
+    assert not blob[3 * hl.matrix_bytes(R, C):].any()
+    for (gq, gs), name in zip(hl.decode_blob(blob, C, R), ("gate", "up", "down")):
+        assert np.array_equal(gq, q[name]), name
+        assert np.array_equal(gs.astype(np.float64), sc[name]), name
