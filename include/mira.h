@@ -226,6 +226,24 @@ int mira_moe_forward(const mira_shape* s, const mira_moe_args* a, hipStream_t st
 int mira_moe_route(const mira_shape* s, const mira_moe_args* a, hipStream_t stream);
 int mira_moe_experts(const mira_shape* s, const mira_moe_args* a, hipStream_t stream);
 
+/* ---- the layer call without a workspace ----------------------------------
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * call as mira_moe_forward, with the library's own scratch array of
+ * MIRA_NOALLOC_SCRATCH_BYTES per device in place of the workspace.  It makes
+ * no allocation of any kind.  a->workspace must be NULL and
+ * a->workspace_bytes 0; every other argument, output and check is that of
+ * mira_moe_forward.  A call whose workspace need, mira_workspace_bytes(s,
+ * n_tokens), exceeds the scratch size fails with MIRA_ERR_WORKSPACE before
+ * any launch (16 MiB covers every decode call of up to 16 tokens at hidden
+ * 4096 and ffn 14336, and prefill calls of up to 64 such tokens).  All calls
+ * on one device share its scratch: calls that overlap in time on one device
+ * (on different streams, or from different threads) race on it and give
+ * undefined results; calls ordered on one stream are safe.  The scratch is
+ * held until the process ends. */
+#define MIRA_NOALLOC_SCRATCH_BYTES (16u << 20)
+int mira_moe_forward_noalloc(const mira_shape* s, const mira_moe_args* a, hipStream_t stream);
+
 /* ---- predictor head (section IV-E) -------------------------------------- */
 typedef struct mira_pred_shape {
   int32_t hidden;      /* C; multiple of 64 */

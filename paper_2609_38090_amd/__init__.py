@@ -18,6 +18,7 @@ from ._binding import (  # noqa: F401
     MIRA_FLAG_SOFTMAX_ALL,
     MIRA_MAX_EXPERTS,
     MIRA_MAX_TOPK,
+    MIRA_NOALLOC_SCRATCH_BYTES,
     MiraError,
     MixtureShape,
     MixtureWeights,
@@ -29,6 +30,7 @@ from ._binding import (  # noqa: F401
     mira_last_error,
     mira_moe_experts,
     mira_moe_forward,
+    mira_moe_forward_noalloc,
     mira_moe_route,
     mira_pack_experts,
     mira_packed_expert_bytes,
@@ -52,6 +54,7 @@ EXPORTED_SYMBOLS = (
     "mira_workspace_bytes",
     "mira_pack_experts",
     "mira_moe_forward",
+    "mira_moe_forward_noalloc",
     "mira_moe_route",
     "mira_moe_experts",
     "mira_predict_workspace_bytes",

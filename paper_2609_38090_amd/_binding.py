@@ -19,6 +19,7 @@ MIRA_FLAG_INT4 = 0x8
 MIRA_DECODE_MAX_TOKENS = 16
 MIRA_MAX_EXPERTS = 256
 MIRA_MAX_TOPK = 16
+MIRA_NOALLOC_SCRATCH_BYTES = 16 << 20
 
 
 class MiraError(RuntimeError):
@@ -212,6 +213,7 @@ def load():
             "mira_pack_experts": (ctypes.c_int, [ctypes.POINTER(_Shape), i32, i32, vp, vp, vp, f32, vp,
                                                  u64, i32, vp]),
             "mira_moe_forward": (ctypes.c_int, [ctypes.POINTER(_Shape), ctypes.POINTER(_Args), vp]),
+            "mira_moe_forward_noalloc": (ctypes.c_int, [ctypes.POINTER(_Shape), ctypes.POINTER(_Args), vp]),
             "mira_moe_route": (ctypes.c_int, [ctypes.POINTER(_Shape), ctypes.POINTER(_Args), vp]),
             "mira_moe_experts": (ctypes.c_int, [ctypes.POINTER(_Shape), ctypes.POINTER(_Args), vp]),
             "mira_predict_workspace_bytes": (sz, [ctypes.POINTER(_PredShape), i32]),
@@ -279,6 +281,11 @@ def mira_pack_experts(shape: MoEShape, n_experts: int, w_dtype: int, w_gate, w_u
 
 def mira_moe_forward(shape: MoEShape, args: MoEArgs, stream=None):
     _check(load().mira_moe_forward(ctypes.byref(shape._c()), ctypes.byref(args._c()), _stream(stream)))
+
+
+def mira_moe_forward_noalloc(shape: MoEShape, args: MoEArgs, stream=None):
+    _check(load().mira_moe_forward_noalloc(ctypes.byref(shape._c()), ctypes.byref(args._c()),
+                                           _stream(stream)))
 
 
 def mira_moe_route(shape: MoEShape, args: MoEArgs, stream=None):

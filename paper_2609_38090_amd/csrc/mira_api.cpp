@@ -490,6 +490,27 @@ int mira_moe_forward(const mira_shape* s, const mira_moe_args* a, hipStream_t st
   return rc ? rc : ok();
 }
 
+int mira_moe_forward_noalloc(const mira_shape* s, const mira_moe_args* a, hipStream_t stream) {
+  int rc = check_shape(s);
+  if (rc) return rc;
+  if (!a) return fail(MIRA_ERR_ARG, "args is NULL");
+  if (a->workspace || a->workspace_bytes)
+    return fail(MIRA_ERR_ARG, "the workspace-free call takes workspace = NULL and workspace_bytes = 0");
+  if (a->n_tokens < 0) return fail(MIRA_ERR_SHAPE, "n_tokens must be >= 0");
+  const size_t need = mira_workspace_bytes(s, a->n_tokens);
+  if (need > MIRA_NOALLOC_SCRATCH_BYTES)
+    return fail(MIRA_ERR_WORKSPACE,
+                "%d tokens need %zu bytes of workspace; the library's scratch holds %u "
+                "(MIRA_NOALLOC_SCRATCH_BYTES): use mira_moe_forward with a workspace",
+                a->n_tokens, need, (unsigned)MIRA_NOALLOC_SCRATCH_BYTES);
+  void* scratch = nullptr;
+  HIP_TRY(mira::noalloc_scratch(&scratch));
+  mira_moe_args b = *a;
+  b.workspace = scratch;
+  b.workspace_bytes = MIRA_NOALLOC_SCRATCH_BYTES;
+  return mira_moe_forward(s, &b, stream);
+}
+
 size_t mira_predict_workspace_bytes(const mira_pred_shape* p, int32_t n_tokens) {
   if (!p || p->group < 1 || p->hidden <= 0 || p->pred_hidden <= 0 || n_tokens < 0) return 0;
   const size_t n = (size_t)(n_tokens / p->group);

@@ -233,6 +233,9 @@ hipError_t launch_mixture(const mira_mixture_shape& p, const mira_mixture_weight
                           const void* x, const float* logits, const int32_t* topk_idx, int T,
                           float* probs, float* alpha, void* ws, hipStream_t st);
 hipError_t launch_set_slot(int32_t* table, int expert, int slot, hipStream_t st);
+// Device address of the library's scratch array on the current device
+// (noalloc.hip), looked up on the first call per device.
+hipError_t noalloc_scratch(void** ptr);
 
 int device_cu_count();
 

@@ -254,3 +254,24 @@ def test_host_pack_int4_matches_header_formulas():
     for (gq, gs), name in zip(hl.decode_blob(out, C, R), ("gate", "up", "down")):
         assert np.array_equal(gq, q[name]), name
         assert np.array_equal(gs.astype(np.float64), sc[name]), name
+
+
+def test_noalloc_forward_argument_checks():
+    """The workspace-free call rejects a caller workspace and a call that would
+    not fit the library's scratch, before touching the GPU."""
+    C, R = 4096, 14336
+    s = mira.MoEShape(C, R, 8, 2, 0, mira.MIRA_BF16)
+    a = mira.MoEArgs(x=0x1000, n_tokens=1, n_slots=8, w_router=0x2000, slot_table=0x3000,
+                     slot_pool=0x10000, slot_stride=mira.mira_packed_expert_bytes(C, R), out=0x4000,
+                     workspace=0x20000, workspace_bytes=1 << 20)
+    with pytest.raises(mira.MiraError) as e:
+        mira.mira_moe_forward_noalloc(s, a, stream=1)
+    assert e.value.code == -1 and "workspace" in mira.mira_last_error()
+    a.workspace, a.workspace_bytes = None, 0
+    big = next(T for T in range(16, 4096, 16)
+               if mira.mira_workspace_bytes(s, T) > mira.MIRA_NOALLOC_SCRATCH_BYTES)
+    a.n_tokens = big
+    with pytest.raises(mira.MiraError) as e:
+        mira.mira_moe_forward_noalloc(s, a, stream=1)
+    assert e.value.code == -4 and "MIRA_NOALLOC_SCRATCH_BYTES" in mira.mira_last_error()
+    assert mira.mira_workspace_bytes(s, 16) <= mira.MIRA_NOALLOC_SCRATCH_BYTES
