@@ -76,14 +76,18 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
-    p.add_argument("--workload", default="mixtral_decode",
-                   choices=["tiny", "mixtral_decode", "mixtral_prefill", "fine_grained", "beam_stack"])
+    p.add_argument("--workload", default=None,
+                   choices=["tiny", "mixtral_decode", "mixtral_prefill", "fine_grained", "beam_stack"],
+                   help="one workload alone; by default mixtral_decode is the headline line and the "
+                        "prefill layers and the beam stack are measured after it (key 'workloads')")
     p.add_argument("--format", default="int8", choices=["int8", "int4"],
                    help="expert format: the paper's shared-scale INT8, or the INT4 variant "
                         "(group-64 fp16 scales; decode workloads only)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-profile", action="store_true", help="skip the per-kernel HIP-event timing")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample")
+    p.add_argument("--extra-cpu-seconds", type=float, default=6.0,
+                   help="budget per oracle leg of the workloads measured after the headline one")
     p.add_argument("--layers", type=int, default=0, help="layers of the beam stack (0 = all)")
     p.add_argument("--stage-slots", type=int, default=8, help="STAGE slots of the beam stack")
     p.add_argument("--drift-steps", type=int, default=36,
@@ -235,16 +239,23 @@ def algorithmic_units(cfg, counts, fmt="int8"):
                 gu_flops=gu_flops, dn_flops=dn_flops)
 
 
-def cpu_baseline(cfg, copy0, budget_s, fmt="int8"):
-    """The oracle, as it stands, on a bounded sample of the same workload."""
+def cpu_baseline(cfg, copy0, budget_s, fmt="int8", legs=(None, 8)):
+    """The oracle, as it stands, on a bounded sample of the same workload.
+
+    The sample is the first tokens of layer copy 0 (up to 64, as many as fit
+    the budget); the experts it needs are packed beforehand (timed apart).
+    The forward over the sample repeats until budget_s is spent, once per
+    leg: None = every BLAS thread the process has, n = BLAS limited to n
+    threads (8 mirrors the paper's 8-core CPU restriction).  Returns the
+    first leg's figures with the others under "legs"."""
     import numpy as np
     import oracle
     from mira_inputs import expert_weights
-    try:
-        from threadpoolctl import threadpool_info
-        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    except Exception:  # pragma: no cover
-        blas_threads = 1
+    from threadpoolctl import threadpool_info, threadpool_limits
+
+    def blas_threads():
+        return max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] + [1])
+
     x = copy0["x"].float().cpu().numpy().astype(np.float64)
     wr = copy0["wr"].float().cpu().numpy().astype(np.float64)
     b = None if copy0["bias"] is None else copy0["bias"].cpu().numpy().astype(np.float64)
@@ -275,28 +286,37 @@ def cpu_baseline(cfg, copy0, budget_s, fmt="int8"):
         def __getitem__(self, e):
             return blobs[e]
 
-    # repeat the forward over the sample until the CPU budget is spent
-    t1 = time.perf_counter()
-    reps = 0
-    while True:
-        oracle.moe_forward(x, wr, b, Blobs(), cfg.k, cfg.C, cfg.R, shared_blobs=shared, tokens=tokens,
-                           fmt=fmt)
-        reps += 1
-        if time.perf_counter() - t1 >= budget_s or reps >= 1000:
-            break
-    fwd_s = time.perf_counter() - t1
+    def leg(threads):
+        with threadpool_limits(limits=threads, user_api="blas"):
+            used = blas_threads()
+            t1 = time.perf_counter()
+            reps = 0
+            while True:
+                oracle.moe_forward(x, wr, b, Blobs(), cfg.k, cfg.C, cfg.R, shared_blobs=shared,
+                                   tokens=tokens, fmt=fmt)
+                reps += 1
+                if time.perf_counter() - t1 >= budget_s or reps >= 1000:
+                    break
+            fwd_s = time.perf_counter() - t1
+        return dict(value=round(reps * len(tokens) / fwd_s, 4), cores=int(used), reps=reps,
+                    seconds=round(fwd_s, 2))
+
+    res = [leg(n) for n in legs]
+    first = res[0]
     return {
-        "value": round(reps * len(tokens) / fwd_s, 4),
+        "value": first["value"],
         "unit": "tokens/s",
-        "cores": int(blas_threads),
+        "cores": first["cores"],
         "kind": "oracle",
         "sample": (f"numpy fp64 oracle forward ({fmt} experts; router, top-k, expert FFN one expert at a "
                    f"time, combine) "
                    f"on the first {len(tokens)} token(s) of layer copy 0 of the same workload; "
                    f"{len(blobs) + len(shared)} experts packed beforehand in {pack_s:.1f} s (not timed); "
-                   f"{reps} forward pass(es) over the sample took {fwd_s:.2f} s; "
-                   f"BLAS threads {blas_threads}, "
+                   f"{first['reps']} forward pass(es) over the sample took {first['seconds']:.2f} s; "
+                   f"BLAS threads {first['cores']}, "
                    f"host CPUs available {len(os.sched_getaffinity(0))}"),
+        "legs": [dict(blas_threads=r["cores"], value=r["value"], reps=r["reps"], seconds=r["seconds"])
+                 for r in res],
     }
 
 
@@ -470,10 +490,12 @@ def run_heads(cfg, n_layers, stack, heads_mix, mix_shape, reps=50):
     return out
 
 
-def run_stack(args, cfg):
+def run_stack(args, cfg, summary=False, cpu_s=None):
     """Beam workload: one decode step of the 8 beams through every layer of the
     stack, experts served from HOT slots, STAGE slots filled ahead of time, or
-    demand copies; reported per mode of the staging policy."""
+    demand copies; reported per mode of the staging policy.  With summary
+    (the default bench run) only the three staging modes of the MLP head are
+    timed, over a few steps, and the fields are returned instead of printed."""
     import torch
     import paper_2609_38090_amd as mira
     from paper_2609_38090_amd.stack import StepStats
@@ -491,8 +513,9 @@ def run_stack(args, cfg):
         torch.cuda.synchronize()
         true_idx.append(stack.idx.cpu().numpy().copy())
         active.append(len(set(true_idx[-1].reshape(-1).tolist())))
-    steps = max(1, min(args.steps, 8))
-    warm = max(1, min(args.warmup, 2))
+    steps = max(1, min(args.steps, 4 if summary else 8))
+    warm = max(1, min(args.warmup, 1 if summary else 2))
+    cpu_s = (0 if args.no_cpu_baseline else args.cpu_seconds) if cpu_s is None else cpu_s
     modes = {}
     prof = {}
     for mode in ("predict", "oracle", "demand"):
@@ -504,10 +527,13 @@ def run_stack(args, cfg):
             mira.mira_profile_enable(True)
             mira.mira_profile_read()
         tot = StepStats()
+        walls = []
         t0 = time.perf_counter()
         for _ in range(steps):
+            t1 = time.perf_counter()
             tot.add(stack.step(mode, true_idx=true_idx))
-        torch.cuda.synchronize()
+            torch.cuda.synchronize()
+            walls.append((time.perf_counter() - t1) * 1e6)
         el = (time.perf_counter() - t0) / steps
         if mode == "predict" and not args.no_profile:
             prof = mira.mira_profile_read()
@@ -523,7 +549,10 @@ def run_stack(args, cfg):
             h2d_gbs_busy=round(per["h2d_bytes"] / max(per["copy_ms"], 1e-9) / 1e6, 1),
             h2d_gbs_wall=round(per["h2d_bytes"] / el / 1e9, 1),
             stall_ms_per_step=round(per["stall_ms"], 3),
+            per_step_us=percentiles(walls),
         )
+    if summary:
+        return stack_summary(cfg, L, fmt, modes, prof, active, steps, warm, build_s, stack, cpu_s)
     # the same policy with the MixtureHead scoring layer l+2
     mix_shape, heads_mix = mixture_heads(cfg, L)
     mlp_shape, heads_mlp = stack.pred_shape, [ld.pred for ld in stack.layers]
@@ -547,16 +576,7 @@ def run_stack(args, cfg):
     stack.set_predictor(mlp_shape, heads_mlp)
     heads = run_heads(cfg, L - 2, stack, heads_mix, mix_shape)
     ms = modes["predict"]["ms_per_step"]
-    gu_bytes = sum(algorithmic_units(cfg, [1] * a + [0] * (cfg.G - a), fmt)["gu_bytes"] for a in active) / L
-    roof = None
-    cnt, tot_ms = prof.get("decode_gateup", (0, 0.0))
-    if cnt:
-        dur = tot_ms / cnt * 1e-3
-        achieved = gu_bytes / dur / 1e9
-        roof = {"bound": "hbm", "kernel": "decode_gateup", "achieved": round(achieved, 1),
-                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": None, "avg_us": round(dur * 1e6, 2),
-                "algorithmic_bytes_per_launch": int(gu_bytes)}
+    roof = stack_roofline(cfg, L, fmt, prof, active)
     line = {
         "metric": METRIC, "value": modes["predict"]["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1,
         "steps": steps, "warmup": warm, "ms_per_step": ms, "higher_is_better": True,
@@ -575,12 +595,231 @@ def run_stack(args, cfg):
     }
     if args.drift_steps > 0:
         line["drift"] = run_drift(cfg, min(L, 8), args.drift_steps, max(1, args.drift_steps // 3), fmt)
-    if not args.no_cpu_baseline:
+    if cpu_s > 0:
         ld = stack.layers[0]
-        line["cpu_baseline"] = cpu_baseline(cfg, dict(x=ld.x, wr=ld.w_router, bias=ld.bias), args.cpu_seconds,
-                                            fmt)
+        line["cpu_baseline"] = cpu_baseline(cfg, dict(x=ld.x, wr=ld.w_router, bias=ld.bias), cpu_s, fmt)
     print(json.dumps(line), flush=True)
     return 0
+
+
+def stack_roofline(cfg, L, fmt, prof, active):
+    """decode_gateup's HBM roofline in the stack: the algorithmic bytes of the
+    average layer's selected experts over the kernel's mean event duration."""
+    gu_bytes = sum(algorithmic_units(cfg, [1] * a + [0] * (cfg.G - a), fmt)["gu_bytes"] for a in active) / L
+    cnt, tot_ms = prof.get("decode_gateup", (0, 0.0))
+    if not cnt:
+        return None
+    dur = tot_ms / cnt * 1e-3
+    achieved = gu_bytes / dur / 1e9
+    return {"bound": "hbm", "kernel": "decode_gateup", "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None, "avg_us": round(dur * 1e6, 2), "algorithmic_bytes_per_launch": int(gu_bytes),
+            "timed_launches": cnt}
+
+
+def stack_summary(cfg, L, fmt, modes, prof, active, steps, warm, build_s, stack, cpu_s):
+    """The beam stack's fields in the default bench line."""
+    import torch
+    res = {"value": modes["predict"]["tokens_per_s"], "unit": "tokens/s", "steps": steps, "warmup": warm,
+           "ms_per_step": modes["predict"]["ms_per_step"], "dtype": "i8",
+           "config": {"workload": cfg.name, "format": fmt, "tokens": cfg.T, "layers": L, "hidden": cfg.C,
+                      "experts": cfg.E, "top_k": cfg.k, "ffn": cfg.R, "resident_per_layer": cfg.resident,
+                      "predictor": f"{cfg.C}->{cfg.pred_hidden}->{cfg.E}",
+                      "experts_selected_per_layer": round(sum(active) / L, 2)},
+           "staging": modes, "setup_s": round(build_s, 1),
+           "kernels_us": {k: round(v[1] / v[0] * 1e3, 2) for k, v in prof.items() if v[0]},
+           "roofline": stack_roofline(cfg, L, fmt, prof, active)}
+    if cpu_s > 0:
+        ld = stack.layers[0]
+        res["cpu_baseline"] = cpu_baseline(cfg, dict(x=ld.x, wr=ld.w_router, bias=ld.bias), cpu_s, fmt)
+    del stack
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
+
+
+def percentiles(us):
+    """p10 / p50 / p90 of a list of per-call times in microseconds."""
+    v = sorted(us)
+    if not v:
+        return None
+    pick = lambda q: v[min(len(v) - 1, int(round(q * (len(v) - 1))))]
+    return {"p10": round(pick(0.1), 2), "p50": round(pick(0.5), 2), "p90": round(pick(0.9), 2),
+            "calls": len(v)}
+
+
+def device_info():
+    """SKU, compute units, HBM and clocks of the GPU the bench runs on."""
+    import subprocess
+    import torch
+    pr = torch.cuda.get_device_properties(0)
+    info = {"name": pr.name, "arch": getattr(pr, "gcnArchName", ""), "compute_units": pr.multi_processor_count,
+            "hbm_gib": round(pr.total_memory / 2 ** 30, 1)}
+    for key, cmd in (("product", ["rocm-smi", "--showproductname", "--json"]),
+                     ("clocks", ["rocm-smi", "--showclocks", "--json"])):
+        try:
+            r = subprocess.run(cmd, capture_output=True, text=True, timeout=20)
+            card = next(iter(json.loads(r.stdout).values()))
+            info[key] = {k.strip(" :"): v for k, v in card.items()}
+        except Exception as e:  # informational only
+            info[key] = f"unavailable ({type(e).__name__})"
+    return info
+
+
+def copy_bandwidth(nbytes=1 << 30, reps=20):
+    """Read + write GB/s of a plain device-to-device copy (the practical
+    ceiling a streaming kernel is compared with), median of reps."""
+    import torch
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    times = []
+    for i in range(reps + 3):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        e1.synchronize()
+        if i >= 3:
+            times.append(e0.elapsed_time(e1) * 1e-3)
+    times.sort()
+    t = times[len(times) // 2]
+    del src, dst
+    torch.cuda.empty_cache()
+    return round(2 * nbytes / t / 1e9, 1)
+
+
+def run_layer(cfg, fmt, steps, warmup, cpu_s, prof_on=True, copy_gbs=None):
+    """One workload's layer call: `steps` timed calls over rotating layer
+    copies, the dominant kernel's roofline from its dispatch-recorded events,
+    per-call p10/p50/p90 from a separate pass with an event pair around each
+    call, and the oracle on a bounded sample (cpu_s seconds per leg; 0 =
+    skip).  Returns the fields of the bench line."""
+    import torch
+    import paper_2609_38090_amd as mira
+
+    # bytes of packed experts one call can touch: at most min(G, T*k + S) experts
+    touched = min(cfg.G, cfg.T * cfg.k + cfg.S) * expert_stride(cfg, fmt)
+    n_copies = max(2, min(8, math.ceil(COLD_BYTES / max(1, touched)) + 1))
+    if cfg.name == "tiny":
+        n_copies = 1
+    copies, stride, act = build_copies(cfg, n_copies, fmt)
+    shape = mira.MoEShape(cfg.C, cfg.R, cfg.E, cfg.k, cfg.S, act, format_flag(fmt))
+    T = cfg.T
+    ws = torch.empty(mira.mira_workspace_bytes(shape, T), dtype=torch.uint8, device="cuda")
+    out = torch.empty((T, cfg.C), dtype=torch.float32, device="cuda")
+    counts = torch.zeros((cfg.G,), dtype=torch.int32, device="cuda")
+    argsets = []
+    for c in copies:
+        argsets.append(mira.MoEArgs(x=c["x"], n_tokens=T, n_slots=cfg.G, w_router=c["wr"],
+                                    router_bias=c["bias"], slot_table=c["table"], slot_pool=c["pool"],
+                                    slot_stride=stride, out=out, expert_counts=counts, workspace=ws,
+                                    workspace_bytes=ws.numel()))
+    stream = torch.cuda.current_stream()
+
+    def step(i):
+        mira.mira_moe_forward(shape, argsets[i % len(argsets)], stream)
+
+    # routed counts of each copy (for the algorithmic byte / flop counts)
+    units = []
+    for i in range(len(argsets)):
+        step(i)
+        torch.cuda.synchronize()
+        units.append(algorithmic_units(cfg, counts.cpu().tolist(), fmt))
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    decode = T <= mira.MIRA_DECODE_MAX_TOKENS
+    dominant = "decode_gateup" if decode else "prefill_gateup"
+
+    def sampled(i):
+        return prof_on and event_step(i, len(argsets))
+
+    if prof_on:
+        # only the dominant kernel carries event records
+        mira.mira_profile_select(dominant)
+        mira.mira_profile_enable(False)
+        mira.mira_profile_read()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        if sampled(i):
+            mira.mira_profile_enable(True)
+            step(i)
+            mira.mira_profile_enable(False)
+        else:
+            step(i)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    prof = mira.mira_profile_read() if prof_on else {}
+    mira.mira_profile_select(None)
+
+    # per-call distribution: a separate pass, one event pair around each call
+    per_call = []
+    n_dist = max(len(argsets) * 4, min(200, steps))
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_dist)]
+    for i, (e0, e1) in enumerate(evs):
+        e0.record(stream)
+        step(i)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    per_call = [e0.elapsed_time(e1) * 1e3 for e0, e1 in evs]
+
+    ms = elapsed * 1e3 / steps
+    value = T / (ms / 1e3)
+    # average algorithmic units per step over the rotation actually timed,
+    # and over the steps whose dominant launch carried the events
+    avg = {k: sum(units[i % len(units)][k] for i in range(steps)) / steps for k in units[0]}
+    samp = [i for i in range(steps) if sampled(i)] or [0]
+    avg_s = {k: sum(units[i % len(units)][k] for i in samp) / len(samp) for k in units[0]}
+    roof = None
+    cnt, tot = prof.get(dominant, (0, 0.0))
+    if cnt:
+        dur = tot / cnt * 1e-3
+        if decode:
+            achieved = avg_s["gu_bytes"] / dur / 1e9
+            roof = {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 1),
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "traffic": traffic_bytes(dominant, cfg.name if fmt == "int8" else f"{cfg.name}_int4"),
+                    "avg_us": round(dur * 1e6, 2),
+                    "algorithmic_bytes_per_launch": int(avg_s["gu_bytes"]),
+                    "timed_launches": cnt}
+            if copy_gbs:
+                roof["frac_of_copy"] = round(achieved / copy_gbs, 4)
+        else:
+            achieved = avg_s["gu_flops"] / dur / 1e12
+            roof = {"bound": "mfma", "kernel": dominant, "achieved": round(achieved, 1),
+                    "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(achieved / BF16_PEAK_TFLOPS, 4),
+                    "traffic": traffic_bytes(dominant, cfg.name),
+                    "avg_us": round(dur * 1e6, 2),
+                    "algorithmic_flops_per_launch": avg_s["gu_flops"],
+                    "achieved_hbm_gbs": round(avg_s["gu_bytes"] / dur / 1e9, 1),
+                    "timed_launches": cnt}
+    step_bytes = avg["gu_bytes"] + avg["dn_bytes"]
+    res = {
+        "value": round(value, 2),
+        "unit": "tokens/s",
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": round(ms, 5),
+        "dtype": "i8" if decode else "bf16",
+        "config": {"workload": cfg.name, "format": fmt, "tokens": T, "hidden": cfg.C, "experts": cfg.E,
+                   "top_k": cfg.k, "ffn": cfg.R, "shared_experts": cfg.S,
+                   "activations": cfg.act, "layer_copies": len(copies),
+                   "experts_touched_per_step": round(avg["active"], 2)},
+        "per_call_us": dict(percentiles(per_call), note="separate pass, an event pair around each call"),
+        "step_packed_gbs": round(step_bytes / (ms / 1e3) / 1e9, 1),
+        "step_tflops": round((avg["gu_flops"] + avg["dn_flops"]) / (ms / 1e3) / 1e12, 2),
+        "kernels_us": {k: round(v[1] / v[0] * 1e3, 2) for k, v in prof.items() if v[0]},
+        "roofline": roof,
+    }
+    if cpu_s > 0:
+        res["cpu_baseline"] = cpu_baseline(cfg, copies[0], cpu_s, fmt)
+    del copies, argsets, ws, out
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
 
 
 def main():
@@ -602,12 +841,12 @@ def main():
     if args.copy_bytes:
         return copy_reference(args.copy_bytes, args.steps)
 
-    import torch
     import paper_2609_38090_amd as mira
     from mira_inputs import CONFIGS
 
     mira.load()
-    cfg = CONFIGS[args.workload]
+    name = args.workload or "mixtral_decode"
+    cfg = CONFIGS[name]
     fmt = args.format
     if fmt == "int4" and cfg.T > mira.MIRA_DECODE_MAX_TOKENS:
         print(json.dumps({"error": "the INT4 variant runs on the decode kernels: use a decode "
@@ -615,138 +854,27 @@ def main():
         return 2
     if cfg.layers > 1:
         return run_stack(args, cfg)
-    # bytes of packed experts one call can touch: at most min(G, T*k + S) experts
-    touched = min(cfg.G, cfg.T * cfg.k + cfg.S) * expert_stride(cfg, fmt)
-    n_copies = max(2, min(8, math.ceil(COLD_BYTES / max(1, touched)) + 1))
-    if cfg.name == "tiny":
-        n_copies = 1
-    copies, stride, act = build_copies(cfg, n_copies, fmt)
-    shape = mira.MoEShape(cfg.C, cfg.R, cfg.E, cfg.k, cfg.S, act, format_flag(fmt))
-    T = cfg.T
-    ws = torch.empty(mira.mira_workspace_bytes(shape, T), dtype=torch.uint8, device="cuda")
-    out = torch.empty((T, cfg.C), dtype=torch.float32, device="cuda")
-    counts = torch.zeros((cfg.G,), dtype=torch.int32, device="cuda")
-    argsets = []
-    for c in copies:
-        argsets.append(mira.MoEArgs(x=c["x"], n_tokens=T, n_slots=cfg.G, w_router=c["wr"],
-                                    router_bias=c["bias"], slot_table=c["table"], slot_pool=c["pool"],
-                                    slot_stride=stride, out=out, expert_counts=counts, workspace=ws,
-                                    workspace_bytes=ws.numel()))
-    pred = None
-    if cfg.pred_hidden:
-        from mira_inputs import predictor_weights
-        w1, b1, w2, b2 = (t.cuda() for t in predictor_weights(cfg, 0, "cpu"))
-        ps = mira.PredShape(cfg.C, cfg.pred_hidden, cfg.E, cfg.pred_group, act)
-        pws = torch.empty(mira.mira_predict_workspace_bytes(ps, T), dtype=torch.uint8, device="cuda")
-        scores = torch.empty((T // cfg.pred_group, cfg.E), dtype=torch.float32, device="cuda")
-        pred = (ps, w1, b1, w2, b2, scores, pws)
-
-    stream = torch.cuda.current_stream()
-
-    def step(i):
-        a = argsets[i % len(argsets)]
-        mira.mira_moe_forward(shape, a, stream)
-        if pred is not None:
-            ps, w1, b1, w2, b2, scores, pws = pred
-            mira.mira_predict(ps, a.x, T, w1, b1, w2, b2, scores, pws, pws.numel(), stream)
-
-    # routed counts of each copy (for the algorithmic byte / flop counts)
-    units = []
-    for i in range(len(argsets)):
-        step(i)
-        torch.cuda.synchronize()
-        units.append(algorithmic_units(cfg, counts.cpu().tolist(), fmt))
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-
-    decode = T <= mira.MIRA_DECODE_MAX_TOKENS
-    dominant = "decode_gateup" if decode else "prefill_gateup"
-    prof_on = not args.no_profile
-
-    def sampled(i):
-        return prof_on and event_step(i, len(argsets))
-
-    if prof_on:
-        # only the dominant kernel carries event records
-        mira.mira_profile_select(dominant)
-        mira.mira_profile_enable(False)
-        mira.mira_profile_read()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        if sampled(i):
-            mira.mira_profile_enable(True)
-            step(i)
-            mira.mira_profile_enable(False)
-        else:
-            step(i)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    prof = {}
-    if prof_on:
-        prof = mira.mira_profile_read()
-
-    ms = elapsed * 1e3 / args.steps
-    value = T / (ms / 1e3)
-    # average algorithmic units per step over the rotation actually timed,
-    # and over the steps whose dominant launch carried the events
-    n = args.steps
-    avg = {k: sum(units[i % len(units)][k] for i in range(n)) / n for k in units[0]}
-    samp = [i for i in range(n) if sampled(i)] or [0]
-    avg_s = {k: sum(units[i % len(units)][k] for i in samp) / len(samp) for k in units[0]}
-    roof = None
-    if prof:
-        if decode:
-            name = dominant
-            cnt, tot = prof.get(name, (0, 0.0))
-            if cnt:
-                dur = tot / cnt * 1e-3
-                achieved = avg_s["gu_bytes"] / dur / 1e9
-                roof = {"bound": "hbm", "kernel": name, "achieved": round(achieved, 1),
-                        "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                        "traffic": traffic_bytes(name, cfg.name if fmt == "int8" else f"{cfg.name}_int4"),
-                        "avg_us": round(dur * 1e6, 2),
-                        "algorithmic_bytes_per_launch": int(avg_s["gu_bytes"]),
-                        "timed_launches": cnt}
-        else:
-            name = "prefill_gateup"
-            cnt, tot = prof.get(name, (0, 0.0))
-            if cnt:
-                dur = tot / cnt * 1e-3
-                achieved = avg_s["gu_flops"] / dur / 1e12
-                roof = {"bound": "mfma", "kernel": name, "achieved": round(achieved, 1),
-                        "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                        "frac": round(achieved / BF16_PEAK_TFLOPS, 4),
-                        "traffic": traffic_bytes(name, cfg.name),
-                        "avg_us": round(dur * 1e6, 2),
-                        "algorithmic_flops_per_launch": avg_s["gu_flops"],
-                        "timed_launches": cnt}
-    step_bytes = avg["gu_bytes"] + avg["dn_bytes"]
-    line = {
-        "metric": METRIC,
-        "value": round(value, 2),
-        "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms, 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "i8" if decode else "bf16",
-        "data": "synthetic",
-        "config": {"workload": cfg.name, "format": fmt, "tokens": T, "hidden": cfg.C, "experts": cfg.E,
-                   "top_k": cfg.k, "ffn": cfg.R, "shared_experts": cfg.S,
-                   "activations": cfg.act, "layer_copies": len(copies),
-                   "experts_touched_per_step": round(avg["active"], 2)},
-        "step_packed_gbs": round(step_bytes / (ms / 1e3) / 1e9, 1),
-        "step_tflops": round((avg["gu_flops"] + avg["dn_flops"]) / (ms / 1e3) / 1e12, 2),
-        "kernels_us": {k: round(v[1] / v[0] * 1e3, 2) for k, v in prof.items() if v[0]},
-        "roofline": roof,
-    }
-    if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(cfg, copies[0], args.cpu_seconds, fmt)
+    cpu_s = 0 if args.no_cpu_baseline else args.cpu_seconds
+    copy_gbs = copy_bandwidth()
+    res = run_layer(cfg, fmt, args.steps, args.warmup, cpu_s, not args.no_profile, copy_gbs)
+    line = {"metric": METRIC, "value": res["value"], "unit": "tokens/s", "n_gpus": 1,
+            "steps": args.steps, "warmup": args.warmup, "ms_per_step": res["ms_per_step"],
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": res["dtype"], "data": "synthetic"}
+    line.update({k: v for k, v in res.items() if k not in line})
+    line["device"] = device_info()
+    line["copy_gbs"] = copy_gbs
+    if args.workload is None:
+        # the default run also measures the prefill layers and the beam stack
+        others = {}
+        extra_cpu = 0 if args.no_cpu_baseline else args.extra_cpu_seconds
+        for other in ("mixtral_prefill", "fine_grained"):
+            print(f"[bench] {other}", file=sys.stderr, flush=True)
+            others[other] = run_layer(CONFIGS[other], "int8", args.steps, args.warmup, extra_cpu,
+                                      not args.no_profile)
+        print("[bench] beam_stack", file=sys.stderr, flush=True)
+        others["beam_stack"] = run_stack(args, CONFIGS["beam_stack"], summary=True, cpu_s=extra_cpu)
+        line["workloads"] = others
     print(json.dumps(line), flush=True)
     return 0
 
