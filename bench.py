@@ -349,14 +349,15 @@ def build_stack(cfg, n_layers, n_stage, hot=None, bias=None, host_all=False, reb
     n_host = sum(cfg.E if host_all else cfg.E - len(ld.hot) for ld in layers)
     host = torch.empty(n_host * stride, dtype=torch.uint8, pin_memory=True)
     tmp = torch.empty(stride, dtype=torch.uint8, device="cuda")
+    hot_slot = stack.hot_slot
     c = 0
     for l, ld in enumerate(layers):
         for e in range(cfg.E):
             wg, wu, wd = expert_weights(cfg, l, e, "cuda")
-            is_hot = e in stack.hot_slot[l]
+            is_hot = e in hot_slot[l]
             mira.mira_pack_experts(pack_shape, 1, mira.MIRA_F32, wg, wu, wd, 1e-8, tmp, stride, 1)
             if is_hot:
-                slot = stack.hot_slot[l][e]
+                slot = hot_slot[l][e]
                 stack.pool[slot * stride:(slot + 1) * stride].copy_(tmp)
             if host_all or not is_hot:
                 blob = host[c * stride:(c + 1) * stride]
@@ -551,6 +552,10 @@ def run_stack(args, cfg, summary=False, cpu_s=None):
             stall_ms_per_step=round(per["stall_ms"], 3),
             per_step_us=percentiles(walls),
         )
+        if tot.cov_total:
+            # mass-weighted coverage of the staged picks: the head's top 2 in
+            # "predict" mode, every true expert of layer l+2 in "oracle" mode
+            modes[mode]["coverage"] = round(tot.coverage, 4)
     if summary:
         return stack_summary(cfg, L, fmt, modes, prof, active, steps, warm, build_s, stack, cpu_s)
     # the same policy with the MixtureHead scoring layer l+2
@@ -572,7 +577,7 @@ def run_stack(args, cfg, summary=False, cpu_s=None):
         hot_hits=per["hot_hits"], stage_hits=per["stage_hits"], misses=per["misses"],
         prefetches=per["prefetches"], prefetch_cached=per["prefetch_cached"],
         prefetch_declined=per["prefetch_declined"], h2d_gb_per_step=round(per["h2d_bytes"] / 1e9, 3),
-        stall_ms_per_step=round(per["stall_ms"], 3))
+        stall_ms_per_step=round(per["stall_ms"], 3), coverage=round(tot.coverage, 4))
     stack.set_predictor(mlp_shape, heads_mlp)
     heads = run_heads(cfg, L - 2, stack, heads_mix, mix_shape)
     ms = modes["predict"]["ms_per_step"]

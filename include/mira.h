@@ -344,6 +344,176 @@ int mira_stage_expert(void* slot_pool, uint64_t slot_stride, int32_t slot,
  * (stream-ordered, so a later forward call on the stream sees it). */
 int mira_set_slot(int32_t* slot_table, int32_t expert, int32_t slot, hipStream_t stream);
 
+/* ---- expert cache runtime (sections IV-C, IV-D, IV-E, IV-F) --------------
+ * The HOT and STAGE regions of the GPU expert cache over one slot pool shared
+ * by the L layers of a model, the lookahead-2 prefetch controller driven by a
+ * predictor head, demand fetches of missing experts, per-expert telemetry and
+ * the bounded HOT rebalancer.  A decode step calls mira_stack_begin_step, then
+ * mira_stack_layer for layers 0..L-1 in order, then mira_stack_end_step.
+ *
+ * One mira_stack_layer call, for layer l, on the stack's compute stream:
+ *  1. mira_moe_route for layer l; the tokens routed to each expert are read
+ *     back to the host (the call waits for that copy: the host decides which
+ *     experts to fetch);
+ *  2. each selected expert is served from its HOT slot, from a STAGE slot
+ *     filled earlier (the compute stream waits for that copy's event only),
+ *     or by a demand copy from its CPU-store blob into a free STAGE slot (a
+ *     miss); the layer's slot-table row is written in stream order;
+ *  3. mira_moe_experts for layer l;
+ *  4. prefetch for layer l + lookahead: the head's stage_per_layer best
+ *     experts (scores summed over the call's token groups, ties to the lower
+ *     index; the head runs on a side stream right after step 1, beside the
+ *     experts), or a given list.  An expert already in HOT or STAGE is a
+ *     skipped prefetch ("cached"), an (expert, layer) pair already staged is
+ *     not copied twice, a prefetch finding no free STAGE slot is declined;
+ *  5. when the layer's telemetry window holds rb_interval tokens, the
+ *     rebalancer swaps at most rb_max_swaps HOT experts for candidates (a
+ *     candidate held in a STAGE slot is relabelled HOT, otherwise it is
+ *     copied from the CPU store into the victim's slot).
+ * A STAGE slot may be taken by a copy when it is free or its layer has passed
+ * in the current step (oldest first); a demand copy may also take the oldest
+ * prefetch for a later layer, never a slot of the current layer.  Small-VRAM
+ * mode frees a layer's STAGE slots right after its experts ran; large-VRAM
+ * mode keeps them (a later step may hit them) until a copy needs the slot.
+ * Every copy runs on the stack's copy stream (default priority) and waits
+ * only for the last kernel that read its slot.
+ *
+ * Memory: the caller owns the slot pool, the slot tables and every CPU-store
+ * blob (page-locked host memory) and keeps them alive until
+ * mira_stack_destroy; the stack allocates its streams, events and small
+ * pinned and device buffers in mira_stack_create and nothing afterwards.  A
+ * stack is used from one host thread at a time. */
+typedef struct mira_stack mira_stack; /* opaque */
+
+#define MIRA_VRAM_LARGE 0
+#define MIRA_VRAM_SMALL 1
+
+typedef struct mira_stack_config {
+  int32_t n_layers;        /* L >= 1 */
+  int32_t n_hot;           /* slots [0, n_hot) of the pool are HOT */
+  int32_t n_stage;         /* slots [n_hot, n_hot + n_stage) are STAGE, >= 0 */
+  int32_t max_tokens;      /* most tokens of one mira_stack_layer call, >= 1 */
+  uint64_t slot_stride;    /* bytes between slots, a multiple of 256 */
+  int32_t vram_mode;       /* MIRA_VRAM_LARGE or MIRA_VRAM_SMALL */
+  int32_t lookahead;       /* the layer staged ahead is l + lookahead (the paper: 2), >= 1 */
+  int32_t stage_per_layer; /* m: experts the head picks per staged layer, >= 1 */
+  int32_t rb_interval;     /* tokens of a layer between rebalancing passes; 0 = no rebalancing */
+  int32_t rb_max_swaps;    /* swaps per layer and pass */
+  int32_t rb_probation;    /* consecutive windows with traffic before a promotion, >= 1 */
+  int32_t rb_margin;       /* a candidate must beat the victim's window volume by this much */
+  float rb_miss_weight;    /* candidate score = routed + miss_weight * CPU-served tokens */
+} mira_stack_config;
+
+/* Counters of the steps since the last mira_stack_end_step (times in ms). */
+typedef struct mira_stack_stats {
+  int64_t hot_hits, stage_hits, misses;          /* selected experts by where they were served */
+  int64_t hot_tokens, stage_tokens, cpu_tokens;  /* routed (token, expert) pairs by tier */
+  int64_t prefetches, prefetch_cached, prefetch_declined;
+  int64_t swaps, promote_copies;                 /* rebalancing swaps; those that copied */
+  int64_t h2d_bytes;                             /* bytes copied host -> device */
+  int64_t cov_hits, cov_total;                   /* Coverage@m: routed pairs of a predicted layer
+                                                    on its predicted experts / all its routed pairs */
+  double copy_ms;                                /* summed durations of the copies */
+  double stall_ms;                               /* time the compute stream waited for copies */
+  double wall_ms;                                /* compute stream, begin to end of the steps */
+} mira_stack_stats;
+
+/* Predictor of layer l + lookahead used by one mira_stack_layer call. */
+#define MIRA_HEAD_NONE 0    /* no prefetch */
+#define MIRA_HEAD_MLP 1     /* mira_predict with mlp_shape and w1, b1, w2, b2 */
+#define MIRA_HEAD_MIXTURE 2 /* mira_predict_mixture with mix_shape and mix (needs the layer's
+                               logits and topk_idx outputs in the layer's args) */
+#define MIRA_HEAD_GIVEN 3   /* stage exactly given[0..n_given) (host array), e.g. the true
+                               experts of the target layer as an upper bound */
+typedef struct mira_stack_head {
+  int32_t kind;
+  int32_t n_given;
+  const int32_t* given;
+  const mira_pred_shape* mlp_shape;
+  const void* w1;
+  const float* b1;
+  const void* w2;
+  const float* b2;
+  const mira_mixture_shape* mix_shape;
+  const mira_mixture_weights* mix;
+  void* workspace; /* the head's device workspace and its size */
+  uint64_t workspace_bytes;
+} mira_stack_head;
+
+/* One entry of the stack's event log (kinds below). */
+#define MIRA_EV_HOT_HIT 0
+#define MIRA_EV_STAGE_HIT 1
+#define MIRA_EV_DEMAND 2       /* a miss: copy from the CPU store */
+#define MIRA_EV_PREDICTED 3    /* the head chose (target, expert) */
+#define MIRA_EV_PREFETCH 4     /* copy issued for (target, expert) */
+#define MIRA_EV_PREFETCH_CACHED 5
+#define MIRA_EV_PREFETCH_DECLINED 6
+#define MIRA_EV_PREFETCH_DROPPED 7 /* a staged prefetch gave its slot to a demand copy */
+#define MIRA_EV_SWAP_RELABEL 8     /* expert promoted to HOT from its STAGE slot */
+#define MIRA_EV_SWAP_COPY 9        /* expert promoted to HOT by a copy into the victim's slot */
+#define MIRA_EV_EVICT 10           /* expert evicted from HOT */
+typedef struct mira_stack_event {
+  int32_t kind;
+  int32_t layer;  /* the layer being run when the event happened */
+  int32_t target; /* the layer the expert belongs to */
+  int32_t expert;
+  int32_t slot;   /* -1 if none */
+  int32_t reserved;
+} mira_stack_event;
+
+/* Create a stack over a caller-owned pool of n_hot + n_stage slots and the
+ * device slot tables [L][E+S] (int32; written only by the stack).  s gives
+ * the layers' shape (all layers share it).  compute is the stream every
+ * layer runs on.  On success *out holds the stack. */
+int mira_stack_create(const mira_stack_config* cfg, const mira_shape* s, void* slot_pool,
+                      int32_t* slot_tables, hipStream_t compute, mira_stack** out);
+int mira_stack_destroy(mira_stack* st);
+
+/* The CPU-store blob of expert e of layer l: `bytes` (<= slot_stride) bytes
+ * of page-locked host memory holding the packed expert. */
+int mira_stack_set_host(mira_stack* st, int32_t layer, int32_t expert, const void* pinned,
+                        uint64_t bytes);
+/* Make HOT slot `slot` (< n_hot) hold expert e of layer l.  With copy = 1 the
+ * expert's CPU-store blob is copied in (copy stream); with copy = 0 the
+ * caller has written the slot's bytes already. */
+int mira_stack_set_hot(mira_stack* st, int32_t layer, int32_t expert, int32_t slot, int32_t copy);
+
+int mira_stack_begin_step(mira_stack* st);
+/* Run layer l (see above).  a carries the layer's inputs, outputs and
+ * workspace; its slot_table, slot_pool, n_slots and slot_stride are taken
+ * from the stack, and a NULL expert_counts is replaced by the stack's own
+ * buffer.  head (may be NULL = MIRA_HEAD_NONE) picks layer l + lookahead's
+ * experts to stage. */
+int mira_stack_layer(mira_stack* st, int32_t layer, const mira_moe_args* a,
+                     const mira_stack_head* head);
+/* Wait for the step's work and add its counters (times included) to *stats
+ * (may be NULL). */
+int mira_stack_end_step(mira_stack* st, mira_stack_stats* stats);
+/* Free every STAGE slot (waits for the stack's queued work first). */
+int mira_stack_reset_stage(mira_stack* st);
+/* Slot holding expert e of layer l as HOT (role 0) or STAGE (role 1), or -1. */
+int32_t mira_stack_find(const mira_stack* st, int32_t layer, int32_t expert, int32_t role);
+/* Move up to max_events logged events (oldest first) to events; *n_events
+ * gets the count.  The log keeps the last 65536 events. */
+int mira_stack_read_events(mira_stack* st, int32_t max_events, mira_stack_event* events,
+                           int32_t* n_events);
+
+/* The rebalancer's decision for one layer (section IV-D), as the stack runs
+ * it, on the host: per expert the tokens routed in the current window and of
+ * those served by a CPU copy, the token clock of its last use (-1 = never),
+ * the routed volumes of up to 8 past windows (hist_len of them, oldest
+ * first, in history[e*8 ...]) and whether it is HOT.  Victims: HOT experts
+ * ordered by (routed, last_use, sum of history, index) ascending.
+ * Candidates: non-HOT experts with routed > 0 whose last probation-1 windows
+ * all had traffic, ordered by score routed + miss_weight * cpu descending,
+ * then index.  The i-th victim and candidate swap while fewer than max_swaps
+ * swaps are planned and score >= victim's routed + margin.  Writes
+ * evict[i], promote[i] for i < *n_swaps. */
+int mira_rebalance_plan(const mira_stack_config* cfg, int32_t n_experts, const int32_t* routed,
+                        const int32_t* cpu, const int64_t* last_use, const int32_t* history,
+                        const int32_t* hist_len, const uint8_t* is_hot, int32_t max_swaps_out,
+                        int32_t* evict, int32_t* promote, int32_t* n_swaps);
+
 /* ---- diagnostics -------------------------------------------------------- */
 /* Description of the last failure on this thread ("" if none). */
 const char* mira_last_error(void);

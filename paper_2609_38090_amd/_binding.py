@@ -20,6 +20,10 @@ MIRA_DECODE_MAX_TOKENS = 16
 MIRA_MAX_EXPERTS = 256
 MIRA_MAX_TOPK = 16
 MIRA_NOALLOC_SCRATCH_BYTES = 16 << 20
+MIRA_VRAM_LARGE, MIRA_VRAM_SMALL = 0, 1
+MIRA_HEAD_NONE, MIRA_HEAD_MLP, MIRA_HEAD_MIXTURE, MIRA_HEAD_GIVEN = 0, 1, 2, 3
+MIRA_STACK_EVENTS = ("hot_hit", "stage_hit", "demand", "predicted", "prefetch", "prefetch_cached",
+                     "prefetch_declined", "prefetch_dropped", "swap_relabel", "swap_copy", "evict")
 
 
 class MiraError(RuntimeError):
@@ -193,6 +197,37 @@ def lib_path() -> str:
     return os.path.join(_PKG, _LIB_NAME)
 
 
+class _StackConfig(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("n_hot", ctypes.c_int32), ("n_stage", ctypes.c_int32),
+                ("max_tokens", ctypes.c_int32), ("slot_stride", ctypes.c_uint64),
+                ("vram_mode", ctypes.c_int32), ("lookahead", ctypes.c_int32),
+                ("stage_per_layer", ctypes.c_int32), ("rb_interval", ctypes.c_int32),
+                ("rb_max_swaps", ctypes.c_int32), ("rb_probation", ctypes.c_int32),
+                ("rb_margin", ctypes.c_int32), ("rb_miss_weight", ctypes.c_float)]
+
+
+STACK_COUNTERS = ("hot_hits", "stage_hits", "misses", "hot_tokens", "stage_tokens", "cpu_tokens",
+                  "prefetches", "prefetch_cached", "prefetch_declined", "swaps", "promote_copies",
+                  "h2d_bytes", "cov_hits", "cov_total")
+
+
+class _StackStats(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in STACK_COUNTERS] + \
+        [("copy_ms", ctypes.c_double), ("stall_ms", ctypes.c_double), ("wall_ms", ctypes.c_double)]
+
+
+class _StackHead(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("n_given", ctypes.c_int32), ("given", ctypes.c_void_p),
+                ("mlp_shape", ctypes.c_void_p), ("w1", ctypes.c_void_p), ("b1", ctypes.c_void_p),
+                ("w2", ctypes.c_void_p), ("b2", ctypes.c_void_p), ("mix_shape", ctypes.c_void_p),
+                ("mix", ctypes.c_void_p), ("workspace", ctypes.c_void_p),
+                ("workspace_bytes", ctypes.c_uint64)]
+
+
+class _StackEvent(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("kind", "layer", "target", "expert", "slot", "reserved")]
+
+
 def load():
     """Load libmira.so (after torch, so both share torch's HIP runtime)."""
     global _LIB
@@ -224,6 +259,19 @@ def load():
                                                     vp, vp, vp, i32, vp, vp, vp, u64, vp]),
             "mira_stage_expert": (ctypes.c_int, [vp, u64, i32, vp, u64, vp, vp]),
             "mira_set_slot": (ctypes.c_int, [vp, i32, i32, vp]),
+            "mira_stack_create": (ctypes.c_int, [ctypes.POINTER(_StackConfig), ctypes.POINTER(_Shape), vp, vp, vp,
+                                                 ctypes.POINTER(vp)]),
+            "mira_stack_destroy": (ctypes.c_int, [vp]),
+            "mira_stack_set_host": (ctypes.c_int, [vp, i32, i32, vp, u64]),
+            "mira_stack_set_hot": (ctypes.c_int, [vp, i32, i32, i32, i32]),
+            "mira_stack_begin_step": (ctypes.c_int, [vp]),
+            "mira_stack_layer": (ctypes.c_int, [vp, i32, ctypes.POINTER(_Args), ctypes.POINTER(_StackHead)]),
+            "mira_stack_end_step": (ctypes.c_int, [vp, ctypes.POINTER(_StackStats)]),
+            "mira_stack_reset_stage": (ctypes.c_int, [vp]),
+            "mira_stack_find": (i32, [vp, i32, i32, i32]),
+            "mira_stack_read_events": (ctypes.c_int, [vp, i32, ctypes.POINTER(_StackEvent), ctypes.POINTER(i32)]),
+            "mira_rebalance_plan": (ctypes.c_int, [ctypes.POINTER(_StackConfig), i32, vp, vp, vp, vp, vp, vp, i32,
+                                                   vp, vp, ctypes.POINTER(i32)]),
             "mira_last_error": (ctypes.c_char_p, []),
             "mira_version": (ctypes.c_char_p, []),
             "mira_profile_enable": (ctypes.c_int, [i32]),
@@ -348,3 +396,104 @@ def mira_profile_read(max_entries: int = 64):
     n = ctypes.c_int32(0)
     _check(lib.mira_profile_read(max_entries, names, counts, ms, ctypes.byref(n)))
     return {names[i].decode(): (int(counts[i]), float(ms[i])) for i in range(min(n.value, max_entries))}
+
+
+# ---- expert cache runtime ---------------------------------------------------
+
+def stack_config(n_layers: int, n_hot: int, n_stage: int, max_tokens: int, slot_stride: int,
+                 vram_mode: int = MIRA_VRAM_LARGE, lookahead: int = 2, stage_per_layer: int = 2,
+                 rb_interval: int = 0, rb_max_swaps: int = 1, rb_probation: int = 2, rb_margin: int = 1,
+                 rb_miss_weight: float = 1.0) -> _StackConfig:
+    return _StackConfig(n_layers, n_hot, n_stage, max_tokens, slot_stride, vram_mode, lookahead,
+                        stage_per_layer, rb_interval, rb_max_swaps, rb_probation, rb_margin, rb_miss_weight)
+
+
+def mira_stack_create(cfg: _StackConfig, shape: MoEShape, slot_pool, slot_tables, compute=None) -> int:
+    h = ctypes.c_void_p(0)
+    _check(load().mira_stack_create(ctypes.byref(cfg), ctypes.byref(shape._c()), _ptr(slot_pool),
+                                    _ptr(slot_tables), _stream(compute), ctypes.byref(h)))
+    return h.value
+
+
+def mira_stack_destroy(st: int):
+    _check(load().mira_stack_destroy(st))
+
+
+def mira_stack_set_host(st: int, layer: int, expert: int, pinned, nbytes: int):
+    _check(load().mira_stack_set_host(st, layer, expert, _ptr(pinned), nbytes))
+
+
+def mira_stack_set_hot(st: int, layer: int, expert: int, slot: int, copy: bool = False):
+    _check(load().mira_stack_set_hot(st, layer, expert, slot, 1 if copy else 0))
+
+
+def mira_stack_begin_step(st: int):
+    _check(load().mira_stack_begin_step(st))
+
+
+def stack_head(kind: int = MIRA_HEAD_NONE, given=None, mlp_shape: "PredShape | None" = None, w1=None,
+               b1=None, w2=None, b2=None, mix_shape: "MixtureShape | None" = None,
+               mix: "MixtureWeights | None" = None, workspace=None, workspace_bytes: int = 0):
+    """A mira_stack_head; the returned tuple keeps the structures it points to alive."""
+    keep = []
+    h = _StackHead(kind=kind, workspace=_ptr(workspace), workspace_bytes=workspace_bytes)
+    if given is not None:
+        arr = (ctypes.c_int32 * max(1, len(given)))(*[int(e) for e in given])
+        keep.append(arr)
+        h.n_given, h.given = len(given), ctypes.cast(arr, ctypes.c_void_p).value
+    if mlp_shape is not None:
+        ps = mlp_shape._c()
+        keep.append(ps)
+        h.mlp_shape = ctypes.addressof(ps)
+        h.w1, h.b1, h.w2, h.b2 = _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2)
+    if mix_shape is not None:
+        ms, mw = mix_shape._c(), mix._c()
+        keep += [ms, mw]
+        h.mix_shape, h.mix = ctypes.addressof(ms), ctypes.addressof(mw)
+    return h, keep
+
+
+def mira_stack_layer(st: int, layer: int, args: MoEArgs, head=None):
+    hp = None if head is None else ctypes.byref(head[0])
+    _check(load().mira_stack_layer(st, layer, ctypes.byref(args._c()), hp))
+
+
+def mira_stack_end_step(st: int) -> dict:
+    s = _StackStats()
+    _check(load().mira_stack_end_step(st, ctypes.byref(s)))
+    return {n: getattr(s, n) for n, _ in _StackStats._fields_}
+
+
+def mira_stack_reset_stage(st: int):
+    _check(load().mira_stack_reset_stage(st))
+
+
+def mira_stack_find(st: int, layer: int, expert: int, role: int) -> int:
+    return int(load().mira_stack_find(st, layer, expert, role))
+
+
+def mira_stack_read_events(st: int, max_events: int = 65536) -> list:
+    """[(kind name, layer, target, expert, slot)] logged since the last read, oldest first."""
+    buf = (_StackEvent * max_events)()
+    n = ctypes.c_int32(0)
+    _check(load().mira_stack_read_events(st, max_events, buf, ctypes.byref(n)))
+    return [(MIRA_STACK_EVENTS[buf[i].kind], buf[i].layer, buf[i].target, buf[i].expert, buf[i].slot)
+            for i in range(n.value)]
+
+
+def mira_rebalance_plan(cfg: _StackConfig, routed, cpu, last_use, history, hist_len, is_hot,
+                        max_swaps_out: int = 64):
+    """Swaps [(evict, promote)] of one rebalancing pass; array arguments are
+    numpy arrays (int32 routed/cpu/hist_len [n], int64 last_use [n], int32
+    history [n][8], uint8 is_hot [n])."""
+    import numpy as np
+    n = len(routed)
+    arrs = [np.ascontiguousarray(a, dtype=t) for a, t in ((routed, np.int32), (cpu, np.int32),
+                                                         (last_use, np.int64), (history, np.int32),
+                                                         (hist_len, np.int32), (is_hot, np.uint8))]
+    ev = np.zeros(max_swaps_out, np.int32)
+    pr = np.zeros(max_swaps_out, np.int32)
+    k = ctypes.c_int32(0)
+    _check(load().mira_rebalance_plan(ctypes.byref(cfg), n, *[a.ctypes.data for a in arrs], max_swaps_out,
+                                      ev.ctypes.data, pr.ctypes.data, ctypes.byref(k)))
+    return [(int(ev[i]), int(pr[i])) for i in range(k.value)]

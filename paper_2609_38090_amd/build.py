@@ -17,7 +17,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libmira.so")
 
-SOURCES = ["route.hip", "decode.hip", "prefill.hip", "pack.hip", "predict.hip", "mixture.hip", "noalloc.hip", "mira_api.cpp"]
+SOURCES = ["route.hip", "decode.hip", "prefill.hip", "pack.hip", "predict.hip", "mixture.hip", "noalloc.hip", "mira_api.cpp", "stack.cpp"]
 ARCH = "gfx950"
 
 COMMON = [

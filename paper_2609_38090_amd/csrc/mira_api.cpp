@@ -364,6 +364,18 @@ void prof_end(const char* name, hipStream_t st) {
   }
 }
 
+int set_error(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int clear_error() { return ok(); }
+
 int device_cu_count() {
   static std::mutex mu;
   static std::map<int, int> cache;

@@ -239,4 +239,10 @@ hipError_t noalloc_scratch(void** ptr);
 
 int device_cu_count();
 
+// The thread-local message behind mira_last_error (mira_api.cpp): set_error
+// stores a formatted message and returns code; clear_error empties it and
+// returns MIRA_OK.
+int set_error(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int clear_error();
+
 }  // namespace mira

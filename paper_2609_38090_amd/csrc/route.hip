@@ -577,6 +577,23 @@ hipError_t launch_decode_prep(const mira_shape& s, const Layout& L, const WsPtr&
   return hipGetLastError();
 }
 
+// A whole slot-table row, passed by value (at most MIRA_MAX_EXPERTS entries).
+struct TableRow {
+  int32_t v[MIRA_MAX_EXPERTS];
+};
+
+__global__ void set_table_kernel(int32_t* table, TableRow row, int n) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) table[i] = row.v[i];
+}
+
+hipError_t launch_set_table(int32_t* table, const int32_t* row, int n, hipStream_t st) {
+  if (n < 1 || n > MIRA_MAX_EXPERTS) return hipErrorInvalidValue;
+  TableRow r;
+  for (int i = 0; i < n; ++i) r.v[i] = row[i];
+  hipLaunchKernelGGL(set_table_kernel, dim3(1), dim3(256), 0, st, table, r, n);
+  return hipGetLastError();
+}
+
 __global__ void set_slot_kernel(int32_t* table, int expert, int slot) { table[expert] = slot; }
 
 hipError_t launch_set_slot(int32_t* table, int expert, int slot, hipStream_t st) {

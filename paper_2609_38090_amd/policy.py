@@ -1,8 +1,10 @@
 """Routing telemetry and the HOT-set rebalancer (paper section IV-D).
 
-Pure host logic, no device calls: the expert stack feeds it the tokens each
-expert received and the tier that served them, and applies its decisions to
-the slot pool.
+Pure host logic, no device calls.  The library's native runtime
+(mira_stack_*, mira_rebalance_plan) makes these decisions on the GPU path;
+this module states them in plain Python as the reference its tests compare
+the native planner with, and carries the settings (RebalanceConfig) the
+Python stack passes to the runtime.
 
 Telemetry (per layer and expert, over the current window of tokens): tokens
 routed to the expert, and of those how many were served from a HOT slot, from
@@ -114,7 +116,7 @@ class Rebalancer:
 
     def plan(self, tel: Telemetry, hot: set) -> list:
         """Swaps for one pass; the caller applies them and closes the window."""
-        victims = sorted(hot, key=lambda e: self.victim_key(tel, e))
+        victims = sorted(hot, key=lambda e: (*self.victim_key(tel, e), e))
         cands = [e for e in range(len(tel.stats))
                  if e not in hot and tel.stats[e].routed > 0 and not self.on_probation(tel, e)]
         cands.sort(key=lambda e: (-self.candidate_score(tel, e), e))

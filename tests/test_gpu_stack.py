@@ -32,7 +32,7 @@ def _head(mira, cfg, l, head):
 
 
 def build(mira, cfg, n_stage, hot=None, bias=None, host_all=False, rebalancer=None, head="mlp",
-          fmt="int8"):
+          fmt="int8", vram_mode="large"):
     from paper_2609_38090_amd.stack import ExpertStack, LayerData
     i4 = fmt == "int4"
     flag = mira.MIRA_FLAG_INT4 if i4 else 0
@@ -47,8 +47,10 @@ def build(mira, cfg, n_stage, hot=None, bias=None, host_all=False, rebalancer=No
     shape = mira.MoEShape(cfg.C, cfg.R, cfg.E, cfg.k, cfg.S, mira.MIRA_BF16, flag)
     ps = (mira.PredShape(cfg.C, cfg.pred_hidden, cfg.E, cfg.pred_group, mira.MIRA_BF16) if head == "mlp" else
           mira.MixtureShape(cfg.C, cfg.E, cfg.k, cfg.k, MIX_PA, MIX_PH, cfg.E, cfg.pred_group, mira.MIRA_BF16))
-    st = ExpertStack(shape, cfg.T, layers, stride, n_stage=n_stage, pred_shape=ps, rebalancer=rebalancer)
+    st = ExpertStack(shape, cfg.T, layers, stride, n_stage=n_stage, pred_shape=ps, rebalancer=rebalancer,
+                     vram_mode=vram_mode)
     pack_shape = mira.MoEShape(cfg.C, cfg.R, 1, 1, flags=flag)
+    hot_slot = st.hot_slot
     for l, ld in enumerate(layers):
         for e in range(cfg.E):
             w = [np.ascontiguousarray(t.numpy()) for t in expert_weights(cfg, l, e, "cpu")]
@@ -57,12 +59,30 @@ def build(mira, cfg, n_stage, hot=None, bias=None, host_all=False, rebalancer=No
             pinned = torch.zeros(stride, dtype=torch.uint8).pin_memory()
             mira.mira_pack_experts(pack_shape, 1, mira.MIRA_F32, w[0].ctypes.data, w[1].ctypes.data,
                                    w[2].ctypes.data, EPS, pinned, stride, 0)
-            if e in st.hot_slot[l]:
-                st.pool[st.hot_slot[l][e] * stride:(st.hot_slot[l][e] + 1) * stride].copy_(pinned)
-            if host_all or e not in st.hot_slot[l]:
+            if e in hot_slot[l]:
+                st.pool[hot_slot[l][e] * stride:(hot_slot[l][e] + 1) * stride].copy_(pinned)
+            if host_all or e not in hot_slot[l]:
                 ld.host[e] = pinned
     torch.cuda.synchronize()
     return st, blobs
+
+
+def oracle_layer(st, cfg, blobs, l, fmt="int8"):
+    """The oracle's output of layer l of the stack on the layer's current input and bias."""
+    ld = st.layers[l]
+    x = ld.x.float().cpu().numpy().astype(np.float64)
+    wr = ld.w_router.float().cpu().numpy().astype(np.float64)
+    b = None if ld.bias is None else ld.bias.cpu().numpy().astype(np.float64)
+    return oracle.moe_forward(x, wr, b, [blobs[l, e] for e in range(cfg.E)], cfg.k, cfg.C, cfg.R, fmt=fmt)
+
+
+def true_routing(mira, st, cfg):
+    out = []
+    for l in range(cfg.layers):
+        mira.mira_moe_route(st.shape, st.args(l))
+        torch.cuda.synchronize()
+        out.append(st.idx.cpu().numpy().copy())
+    return out
 
 
 def run(st, mode, true_idx=None):
@@ -124,9 +144,10 @@ def test_rebalancer_tracks_drift_without_changing_outputs(mira):
     hot0 = lambda l: drift_hot(cfg, l, 0, cfg.resident)  # noqa: E731
     b0 = lambda l: drift_bias(cfg, l, 0)  # noqa: E731
     fixed, _ = build(mira, cfg, 4, hot=hot0, bias=b0, host_all=True)
-    moving, _ = build(mira, cfg, 4, hot=hot0, bias=b0, host_all=True,
-                      rebalancer=Rebalancer(RebalanceConfig(interval=32, max_swaps=1, probation=2)))
+    moving, blobs = build(mira, cfg, 4, hot=hot0, bias=b0, host_all=True,
+                          rebalancer=Rebalancer(RebalanceConfig(interval=32, max_swaps=1, probation=2)))
     swaps = 0
+    kinds = set()
     for s in range(24):
         ep = s // 6
         for st in (fixed, moving):
@@ -136,9 +157,14 @@ def test_rebalancer_tracks_drift_without_changing_outputs(mira):
         a, _ = run(fixed, "demand")
         b, stats = run(moving, "demand" if s % 2 else "predict")
         swaps += stats.swaps
+        kinds |= {ev[0] for ev in moving.events()}
         for l in range(cfg.layers):
             assert np.array_equal(a[l], b[l]), (s, l)
+        if s in (11, 23):  # after swaps: the rebalanced stack against the oracle
+            for l in range(cfg.layers):
+                assert_ffn_close(b[l], oracle_layer(moving, cfg, blobs, l)["out"], f"step {s} layer {l}")
     assert swaps > 0
+    assert "evict" in kinds and kinds & {"swap_relabel", "swap_copy"}
     # the rebalanced HOT sets hold more of the last period's popular experts
     last = [set(drift_hot(cfg, l, 3, cfg.resident)) for l in range(cfg.layers)]
     got_fixed = sum(len(fixed.hot_set(l) & last[l]) for l in range(cfg.layers))
@@ -155,15 +181,7 @@ def test_stack_with_mixture_head_stages_its_top_experts(mira):
     st, _ = build(mira, cfg, 8, head="mixture")
     dem, _ = run(st, "demand")
     st.reset_stage()
-    requested = []
-    orig = st._stage
-
-    def spy(tgt, e, *a, **kw):
-        if not a[1]:  # a prefetch, not a demand copy
-            requested.append((tgt, e))
-        return orig(tgt, e, *a, **kw)
-
-    st._stage = spy
+    st.events()  # drop the earlier steps' log
     routing = {}
 
     def grab(l, out):
@@ -171,6 +189,8 @@ def test_stack_with_mixture_head_stages_its_top_experts(mira):
 
     stats = st.step("predict", on_layer=grab)
     torch.cuda.synchronize()
+    log = st.events()
+    requested = [(t, e) for (kind, l, t, e, slot) in log if kind == "predicted"]
     for l in range(cfg.layers):
         assert np.array_equal(routing[l][2].cpu().numpy(), dem[l]), l
     assert stats.prefetches + stats.prefetch_cached + stats.prefetch_declined == 2 * (cfg.layers - 2)
@@ -186,6 +206,118 @@ def test_stack_with_mixture_head_stages_its_top_experts(mira):
             continue
         want = set(order[:2].tolist())
         got = {e for (t, e) in requested if t == l + 2}
-        assert got == want - st.hot_set(l + 2), (l, got, want)
+        assert got == want, (l, got, want)
+        # every pick was staged, found cached, or declined
+        fate = {e: kind for (kind, ll, t, e, slot) in log if t == l + 2 and ll == l and
+                kind in ("prefetch", "prefetch_cached", "prefetch_declined")}
+        assert set(fate) == want
+        for e in want & st.hot_set(l + 2):
+            assert fate[e] == "prefetch_cached"
         checked += 1
     assert checked > 0
+
+
+def test_small_vram_mode_frees_stage_slots_after_their_layer(mira):
+    """Small-VRAM mode (section IV-C): a STAGE slot is released right after its
+    layer, so no slot holds an expert once the step is over and a second step
+    finds nothing staged; outputs equal the large-VRAM stack's and the oracle's."""
+    cfg = SMALL_STACK
+    small, blobs = build(mira, cfg, 4, vram_mode="small")
+    large, _ = build(mira, cfg, 4)
+    true_idx = true_routing(mira, small, cfg)
+    for mode in ("oracle", "demand", "predict"):
+        for rep in range(2):
+            a, sa = run(small, mode, true_idx)
+            b, sb = run(large, mode, true_idx)
+            for l in range(cfg.layers):
+                assert np.array_equal(a[l], b[l]), (mode, rep, l)
+            assert all(small.staged(l, e) < 0 for l in range(cfg.layers) for e in range(cfg.E))
+            if mode == "demand":
+                assert sa.stage_hits == 0
+    for l in range(cfg.layers):
+        assert_ffn_close(a[l], oracle_layer(small, cfg, blobs, l)["out"], f"small layer {l}")
+
+
+def test_stage_capacity_zero_with_every_expert_hot(mira):
+    """No STAGE slot at all: with every expert HOT nothing is ever copied, each
+    prediction is a skipped ("cached") prefetch, and outputs match the oracle."""
+    cfg = SMALL_STACK
+    st, blobs = build(mira, cfg, 0, hot=lambda l: list(range(cfg.E)))
+    st.events()
+    outs, stats = run(st, "predict")
+    log = st.events()
+    assert stats.misses == 0 and stats.stage_hits == 0 and stats.h2d_bytes == 0
+    assert stats.prefetches == 0 and stats.prefetch_declined == 0
+    assert stats.prefetch_cached == 2 * (cfg.layers - 2)
+    assert {k for (k, *_ ) in log} <= {"hot_hit", "predicted", "prefetch_cached"}
+    for l in range(cfg.layers):
+        assert_ffn_close(outs[l], oracle_layer(st, cfg, blobs, l)["out"], f"layer {l}")
+
+
+def test_stage_capacity_one_declines_and_drops_prefetches(mira):
+    """One STAGE slot beside 7 of 8 experts HOT per layer.  The non-HOT
+    expert of layers 0 and 1 is one they do not select, that of layers 2, 3
+    and 4 one they do.  In oracle mode, layer 0 prefetches layer 2's expert
+    into the slot; at layer 1 the slot still holds that prefetch for the next
+    layer, so the prefetch for layer 3 is declined; layer 2 hits its staged
+    expert; later demand copies may take a prefetch for a later layer (it is
+    dropped).  Outputs equal demand fetching and the oracle."""
+    cfg = SMALL_STACK
+    probe, _ = build(mira, cfg, 0, hot=lambda l: list(range(cfg.E)))
+    sel = [set(r.reshape(-1).tolist()) for r in true_routing(mira, probe, cfg)]
+    del probe
+    if any(len(sel[l]) == cfg.E for l in (0, 1)):
+        pytest.skip("layers 0 and 1 select every expert at this seed")
+    cold = [min(set(range(cfg.E)) - sel[l]) if l < 2 else min(sel[l]) for l in range(cfg.layers)]
+    st, blobs = build(mira, cfg, 1, hot=lambda l: [e for e in range(cfg.E) if e != cold[l]], host_all=True)
+    true_idx = true_routing(mira, st, cfg)
+    dem, _ = run(st, "demand")
+    st.reset_stage()
+    st.events()
+    outs, stats = run(st, "oracle", true_idx)
+    log = st.events()
+    assert ("prefetch", 0, 2, cold[2], st.n_hot) in log
+    assert ("prefetch_declined", 1, 3, cold[3], -1) in log
+    assert ("stage_hit", 2, 2, cold[2], st.n_hot) in log
+    assert stats.prefetch_declined >= 1 and stats.stage_hits >= 1
+    for rep in range(2):
+        for l in range(cfg.layers):
+            assert np.array_equal(outs[l], dem[l]), (rep, l)
+        outs, _ = run(st, "oracle", true_idx)
+    for l in range(cfg.layers):
+        assert_ffn_close(dem[l], oracle_layer(st, cfg, blobs, l)["out"], f"layer {l}")
+
+
+def test_coverage_of_the_mlp_head_matches_the_oracle(mira):
+    """Coverage@m (section VI-B, mass-weighted): the runtime counts, for each
+    layer l+2 it predicted, the routed pairs landing on the head's m picks.
+    Its totals equal the sum over the picks it logged, and on every layer
+    whose oracle top-m ranking has a clear gap the picks are the oracle head's
+    and the covered mass is the oracle's coverage_at_k against the true
+    routing."""
+    cfg = SMALL_STACK
+    st, blobs = build(mira, cfg, 8)
+    true_idx = true_routing(mira, st, cfg)
+    st.events()
+    _, stats = run(st, "predict")
+    log = st.events()
+    m = st.stage_per_layer
+    num = tot = checked = 0
+    for l in range(cfg.layers - 2):
+        counts = np.bincount(true_idx[l + 2].reshape(-1), minlength=cfg.E)
+        picks = [e for (k, ll, t, e, slot) in log if k == "predicted" and t == l + 2]
+        assert len(picks) == m
+        num += int(counts[picks].sum())
+        tot += int(counts.sum())
+        w1, b1, w2, b2 = (t.float().cpu().numpy() for t in st.layers[l].pred)
+        x = st.layers[l].x.float().cpu().numpy().astype(np.float64)
+        sc = oracle.predictor_scores(x, cfg.pred_group, w1, b1, w2, b2).sum(axis=0)
+        srt = np.sort(sc)[::-1]
+        if srt[m - 1] - srt[m] < 1e-5:
+            continue
+        assert set(picks) == set(np.argsort(-sc, kind="stable")[:m].tolist()), l
+        assert int(counts[picks].sum()) == round(oracle.coverage_at_k(sc, counts, m) * counts.sum()), l
+        checked += 1
+    assert (stats.cov_hits, stats.cov_total) == (num, tot)
+    assert checked > 0
+    print(f"Coverage@{m} of the untrained MLP head: {stats.coverage:.3f} ({checked} layers checked)")

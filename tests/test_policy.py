@@ -63,3 +63,48 @@ def test_victim_order_uses_recency_then_frequency():
     tel.stats[1].last_use = 1      # 1 was used later than 0
     (sw,) = rb.plan(tel, {0, 1})
     assert sw.evict == 0 and sw.promote == 3
+
+
+def _random_telemetry(rng, n, windows):
+    from paper_2609_38090_amd.policy import Telemetry
+    tel = Telemetry(n)
+    for w in range(windows):
+        traffic = {e: int(rng.integers(0, 6)) if rng.random() < 0.6 else 0 for e in range(n)}
+        tiers = {e: ["hot", "stage", "cpu"][int(rng.integers(0, 3))] for e in range(n)}
+        for e, k in traffic.items():
+            if k:
+                tel.record(e, k, tiers[e])
+        tel.advance(int(rng.integers(1, 9)))
+        if w < windows - 1:
+            tel.close_window()
+    return tel
+
+
+def test_native_planner_matches_the_reference_policy():
+    """mira_rebalance_plan (the planner the native runtime runs) makes the same
+    swaps as policy.Rebalancer.plan on random telemetry, settings and HOT sets."""
+    import numpy as np
+    import paper_2609_38090_amd as mira
+    rng = np.random.default_rng(7)
+    differ = 0
+    for case in range(400):
+        n = int(rng.integers(2, 17))
+        cfg = RebalanceConfig(interval=8, max_swaps=int(rng.integers(0, 4)), probation=int(rng.integers(1, 4)),
+                              miss_weight=float(rng.choice([0.0, 0.5, 1.0, 2.0])), margin=int(rng.integers(0, 3)))
+        tel = _random_telemetry(rng, n, int(rng.integers(1, 12)))
+        hot = set(int(e) for e in rng.choice(n, int(rng.integers(0, n + 1)), replace=False))
+        want = [(s.evict, s.promote) for s in Rebalancer(cfg).plan(tel, hot)]
+        hist = np.zeros((n, 8), np.int32)
+        hl = np.zeros(n, np.int32)
+        for e, st in enumerate(tel.stats):
+            h = list(st.history)
+            hist[e, :len(h)] = h
+            hl[e] = len(h)
+        c = mira.stack_config(1, 1, 0, 1, 256, rb_interval=cfg.interval, rb_max_swaps=cfg.max_swaps,
+                              rb_probation=cfg.probation, rb_margin=cfg.margin, rb_miss_weight=cfg.miss_weight)
+        got = mira.mira_rebalance_plan(c, [s.routed for s in tel.stats], [s.cpu for s in tel.stats],
+                                       [s.last_use for s in tel.stats], hist, hl,
+                                       [1 if e in hot else 0 for e in range(n)])
+        assert got == want, (case, got, want)
+        differ += bool(want)
+    assert differ > 50  # enough cases actually swap
