@@ -297,3 +297,18 @@ def test_decode_one_shot_matches_two_phase_and_prefill_routing(mira, cfg, T):
     for key in ("idx", "w", "logits", "counts", "offsets", "order"):
         assert np.array_equal(one[key], pre[key]), key
     run_and_check(lay, res=one)
+
+
+@pytest.mark.parametrize("cfg,T", [(SMALL_BF16, 1), (SMALL_BF16, 3), (SMALL_BF16, 5), (SMALL_FG, 1),
+                                   (SMALL_F32, 2)])
+def test_decode_results_independent_of_workspace_contents(mira, cfg, T):
+    """Nothing in the workspace needs to start in a given state: a workspace
+    of 0xFF bytes, one of 0xA5, one of zeros and the same workspace reused
+    give bit-identical results that match the oracle."""
+    lay = Layer(cfg, T=T)
+    ref = lay.run(ws_fill=0x00)
+    for fill in (0xFF, 0xA5, None):
+        got = lay.run(ws_fill=fill)
+        for key in ref:
+            assert np.array_equal(got[key], ref[key]), (fill, key)
+    run_and_check(lay, res=ref)
