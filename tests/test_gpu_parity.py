@@ -312,3 +312,30 @@ def test_decode_results_independent_of_workspace_contents(mira, cfg, T):
         for key in ref:
             assert np.array_equal(got[key], ref[key]), (fill, key)
     run_and_check(lay, res=ref)
+
+
+def test_predictor_groups_are_independent(mira):
+    """A group's scores do not depend on the other groups of the call (1, 4
+    or 5 groups give bit-identical scores for the groups they share), from a
+    workspace of 0xFF bytes and when the workspace is reused; all match the
+    oracle."""
+    cfg = CONFIGS["beam_stack"]
+    x = activations(cfg, 4, "cpu", T=40)
+    w1, b1, w2, b2 = predictor_weights(cfg, 4, "cpu")
+    b1 = torch.randn(b1.shape, generator=torch.Generator().manual_seed(2)) * 0.1
+    b2 = torch.randn(b2.shape, generator=torch.Generator().manual_seed(3)) * 0.1
+    dev = [t.cuda() for t in (w1, b1, w2, b2)]
+    p = mira.PredShape(cfg.C, cfg.pred_hidden, cfg.E, cfg.pred_group, mira.MIRA_BF16)
+    out = {}
+    for T in (32, 40, 8):
+        ws = torch.full((mira.mira_predict_workspace_bytes(p, T),), 0xFF, dtype=torch.uint8, device="cuda")
+        sc = torch.zeros((T // cfg.pred_group, cfg.E), dtype=torch.float32, device="cuda")
+        for _ in range(2):  # the second call reuses the workspace
+            mira.mira_predict(p, x[:T].cuda(), T, *dev[:2], *dev[2:], sc, ws, ws.numel())
+        torch.cuda.synchronize()
+        out[T] = sc.cpu().numpy()
+        ref = oracle.predictor_scores(x[:T].float().numpy(), cfg.pred_group, w1.float().numpy(), b1.numpy(),
+                                      w2.float().numpy(), b2.numpy())
+        assert np.max(np.abs(out[T] - ref)) < 1e-4, T
+    assert np.array_equal(out[32], out[40][:4])
+    assert np.array_equal(out[8], out[40][:1])
