@@ -44,11 +44,13 @@ PROF_EVERY = 8  # steps timed with events: one layer-copy rotation in every 8
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 TRAFFIC = {
     ("decode_gateup", "mixtral_decode"): dict(sources=("decode.hip", "decode_dev.h", "int4_format.h"),
-                                               sha="138b8c3d2a45bbb9", fetch_kib=114823.3, write_kib=98.0),
+                                               sha="7dea4bd328214dd8", fetch_kib=114822.7, write_kib=98.0),
     ("decode_gateup", "mixtral_decode_int4"): dict(sources=("decode.hip", "decode_dev.h", "int4_format.h"),
-                                                    sha="138b8c3d2a45bbb9", fetch_kib=61050.7, write_kib=98.0),
-    ("prefill_gateup", "mixtral_prefill"): dict(sources=("prefill.hip",), sha="d36f59a2f3ec2d7a",
-                                                 fetch_kib=601701.1, write_kib=38364.3),
+                                                    sha="7dea4bd328214dd8", fetch_kib=61050.4, write_kib=98.0),
+    ("prefill_gateup", "mixtral_prefill"): dict(sources=("prefill.hip",), sha="a1fac0bd38061bf5",
+                                                 fetch_kib=599131.7, write_kib=37599.8),
+    ("prefill_gateup", "fine_grained"): dict(sources=("prefill.hip",), sha="a1fac0bd38061bf5",
+                                              fetch_kib=290115.5, write_kib=57402.6),
 }
 
 
@@ -653,13 +655,19 @@ def percentiles(us):
             "calls": len(v)}
 
 
-def device_info():
-    """SKU, compute units, HBM and clocks of the GPU the bench runs on."""
+def profiler_attached():
+    """True under rocprofv3: its preloaded library initialises the GPU in
+    every process it starts, so a child program must not be spawned then."""
+    return any(k.startswith("ROCPROF") for k in os.environ) or "rocprofiler" in os.environ.get("LD_PRELOAD", "")
+
+
+def smi_info():
+    """Product name and clocks from rocm-smi.  Runs a child process, so it is
+    called before this process touches the GPU, and skipped under a profiler."""
     import subprocess
-    import torch
-    pr = torch.cuda.get_device_properties(0)
-    info = {"name": pr.name, "arch": getattr(pr, "gcnArchName", ""), "compute_units": pr.multi_processor_count,
-            "hbm_gib": round(pr.total_memory / 2 ** 30, 1)}
+    if profiler_attached():
+        return {"product": "skipped (profiler attached)", "clocks": "skipped (profiler attached)"}
+    info = {}
     for key, cmd in (("product", ["rocm-smi", "--showproductname", "--json"]),
                      ("clocks", ["rocm-smi", "--showclocks", "--json"])):
         try:
@@ -668,6 +676,16 @@ def device_info():
             info[key] = {k.strip(" :"): v for k, v in card.items()}
         except Exception as e:  # informational only
             info[key] = f"unavailable ({type(e).__name__})"
+    return info
+
+
+def device_info(smi):
+    """SKU, compute units, HBM and clocks of the GPU the bench runs on."""
+    import torch
+    pr = torch.cuda.get_device_properties(0)
+    info = {"name": pr.name, "arch": getattr(pr, "gcnArchName", ""), "compute_units": pr.multi_processor_count,
+            "hbm_gib": round(pr.total_memory / 2 ** 30, 1)}
+    info.update(smi)
     return info
 
 
@@ -846,6 +864,7 @@ def main():
     if args.copy_bytes:
         return copy_reference(args.copy_bytes, args.steps)
 
+    smi = smi_info()  # before anything touches the GPU
     import paper_2609_38090_amd as mira
     from mira_inputs import CONFIGS
 
@@ -867,7 +886,7 @@ def main():
             "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
             "dtype": res["dtype"], "data": "synthetic"}
     line.update({k: v for k, v in res.items() if k not in line})
-    line["device"] = device_info()
+    line["device"] = device_info(smi)
     line["copy_gbs"] = copy_gbs
     if args.workload is None:
         # the default run also measures the prefill layers and the beam stack
