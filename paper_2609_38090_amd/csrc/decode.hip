@@ -114,18 +114,22 @@ __global__ __launch_bounds__(256, 2) void decode_gateup_xl_kernel(int C, int R, 
 // per-64-row exponents of H', multiplied by the combine weight of each
 // (token, expert) pair and summed per token in a fixed order (expert list
 // order inside a wave, then wave order), so the result is deterministic.
+// H' has HD digits per entry (h_digits): an operand of 16 columns holds 5
+// tokens of three digits or 8 of two (column r16 = token r16/HD of the
+// group, digit r16%HD), and NG groups cover that many tokens per group.
 // ---------------------------------------------------------------------------
-template <int NG, int KS, bool I4>
+template <int NG, int KS, bool I4, int HD>
 __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
     int C, int R, int T, int max_active, ExpertPool ep, const DecodeWork* __restrict__ work,
     const int8_t* __restrict__ hdig, const int32_t* __restrict__ hexp, float* __restrict__ out) {
+  constexpr int TPG = h_tok_per_group(HD);
   __shared__ float part[KS][MIRA_DECODE_MAX_TOKENS][16];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   for (int i = tid; i < KS * MIRA_DECODE_MAX_TOKENS * 16; i += 64 * KS) (&part[0][0][0])[i] = 0.f;
   __syncthreads();
 
   const int r16 = lane & 15, kg = lane >> 4;
-  const int m = r16 / 3, d = r16 - 3 * m;
+  const int m = r16 / HD, d = r16 - HD * m;
   const int nks = R / 64;
   // k-steps per wave; even for INT4, whose loads cover two k-steps
   const int spw = I4 ? (((nks + KS - 1) / KS + 1) & ~1) : (nks + KS - 1) / KS;
@@ -152,10 +156,10 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
     bool bv[NG];
 #pragma unroll
     for (int cg = 0; cg < NG; ++cg) {
-      const int i = cg * kTokPerGroup + m;
-      bv[cg] = r16 < 3 * kTokPerGroup && i < n;
+      const int i = cg * TPG + m;
+      bv[cg] = r16 < HD * TPG && i < n;
       const size_t pos = (size_t)off + (bv[cg] ? i : 0);
-      bp[cg] = hdig + (pos * kDigits + d) * R + kg * 16;
+      bp[cg] = hdig + (pos * HD + d) * R + kg * 16;
       hx[cg] = hexp + pos * nks;
     }
     float facc[NG][4];
@@ -227,14 +231,14 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
     }
 #pragma unroll
     for (int cg = 0; cg < NG; ++cg) {
-      const int ti = cg * kTokPerGroup + m;
+      const int ti = cg * TPG + m;
       const bool lead = d == 0 && bv[cg];
       const int t = lead ? wk.tok[ti] : 0;
       const float wgt = lead ? wk.w[ti] : 0.f;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float v = facc[cg][i] + __shfl_down(facc[cg][i], 1, 64) +
-                        __shfl_down(facc[cg][i], 2, 64);
+        float v = facc[cg][i] + __shfl_down(facc[cg][i], 1, 64);
+        if constexpr (HD == 3) v += __shfl_down(facc[cg][i], 2, 64);
         if (lead) part[wave][t][kg * 4 + i] += wgt * v;
       }
     }
@@ -253,30 +257,50 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
 // batches of half the size (INT4 down 20.5 -> 18.0 us, INT8 unchanged)
 constexpr int kDownKS = 16;
 
-template <int NG, bool I4>
+template <int NG, bool I4, int HD>
 static void launch_decode_down_ng(const Layout& L, const WsPtr& w, const ExpertPool& ep,
                                   float* out, hipStream_t st) {
-  launch_timed("decode_down", (decode_down_kernel<NG, kDownKS, I4>), dim3(L.C / 16),
+  launch_timed("decode_down", (decode_down_kernel<NG, kDownKS, I4, HD>), dim3(L.C / 16),
                dim3(64 * kDownKS), 0, st, L.C, L.R, L.T, decode_max_active(L), ep, w.dwork, w.hdig,
                w.hexp, out);
 }
 
 template <int NG, bool I4>
-static void launch_decode_ffn(const Layout& L, const WsPtr& w, const ExpertPool& ep, float* out,
-                              hipStream_t st) {
+static void launch_decode_gateup(const Layout& L, const WsPtr& w, const ExpertPool& ep,
+                                 hipStream_t st) {
   const int nrb = L.R / kBlk;
   const int max_active = decode_max_active(L);
   if constexpr (I4 && NG == 1) {
     if (L.C <= kXlMaxC) {
       launch_timed("decode_gateup", decode_gateup_xl_kernel, dim3(max_active * nrb), dim3(256), 0, st,
                    L.C, L.R, ep, w.dwork, w.xdig, w.hdig, w.hexp);
-      launch_decode_down_ng<NG, I4>(L, w, ep, out, st);
       return;
     }
   }
   launch_timed("decode_gateup", (decode_gateup_kernel<NG, I4>), dim3(max_active * nrb),
                dim3(256), 0, st, L.C, L.R, ep, w.dwork, w.xdig, w.hdig, w.hexp);
-  launch_decode_down_ng<NG, I4>(L, w, ep, out, st);
+}
+
+template <bool I4>
+static void launch_decode_ffn(const Layout& L, const WsPtr& w, const ExpertPool& ep, float* out,
+                              hipStream_t st) {
+  // token groups of an expert (each holds at most T tokens): 5 tokens per x
+  // operand; H' in three digits for one x group (5 tokens per operand),
+  // else in two (8 tokens per operand)
+  const int ng = (L.T + kTokPerGroup - 1) / kTokPerGroup;
+  switch (ng) {
+    case 1: launch_decode_gateup<1, I4>(L, w, ep, st); break;
+    case 2: launch_decode_gateup<2, I4>(L, w, ep, st); break;
+    case 3: launch_decode_gateup<3, I4>(L, w, ep, st); break;
+    default: launch_decode_gateup<4, I4>(L, w, ep, st); break;
+  }
+  static_assert(MIRA_DECODE_MAX_TOKENS <= 2 * h_tok_per_group(2), "two H' groups cover a decode call");
+  if (ng == 1)
+    launch_decode_down_ng<1, I4, 3>(L, w, ep, out, st);
+  else if (L.T <= h_tok_per_group(2))
+    launch_decode_down_ng<1, I4, 2>(L, w, ep, out, st);
+  else
+    launch_decode_down_ng<2, I4, 2>(L, w, ep, out, st);
 }
 
 hipError_t launch_decode(const mira_shape& s, const Layout& L, const WsPtr& w, const void* x,
@@ -284,22 +308,10 @@ hipError_t launch_decode(const mira_shape& s, const Layout& L, const WsPtr& w, c
   (void)x;  // x enters through the fixed-point digits written by decode_prep_kernel
   const int T = L.T;
   if (T == 0) return hipSuccess;
-  const int ng = (T + kTokPerGroup - 1) / kTokPerGroup;  // every group holds <= T tokens
-  if (s.flags & MIRA_FLAG_INT4) {
-    switch (ng) {
-      case 1: launch_decode_ffn<1, true>(L, w, ep, out, st); break;
-      case 2: launch_decode_ffn<2, true>(L, w, ep, out, st); break;
-      case 3: launch_decode_ffn<3, true>(L, w, ep, out, st); break;
-      default: launch_decode_ffn<4, true>(L, w, ep, out, st); break;
-    }
-  } else {
-    switch (ng) {
-      case 1: launch_decode_ffn<1, false>(L, w, ep, out, st); break;
-      case 2: launch_decode_ffn<2, false>(L, w, ep, out, st); break;
-      case 3: launch_decode_ffn<3, false>(L, w, ep, out, st); break;
-      default: launch_decode_ffn<4, false>(L, w, ep, out, st); break;
-    }
-  }
+  if (s.flags & MIRA_FLAG_INT4)
+    launch_decode_ffn<true>(L, w, ep, out, st);
+  else
+    launch_decode_ffn<false>(L, w, ep, out, st);
   return hipGetLastError();
 }
 

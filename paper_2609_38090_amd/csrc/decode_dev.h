@@ -33,12 +33,16 @@ __host__ __device__ constexpr int dec_unroll(int ng) { return ng == 1 ? 16 : ng 
 // H' of one 64-row block as fixed-point digits with one exponent per token
 // and block: bmax holds each wave's per-token maxima of |hv|; lane (kg, r16)
 // holds rows rb*64 + wave*16 + kg*4 + i of token column r16 (lead lanes).
+// With HD = 3 digits H' has kFixBits bits against the block maximum, with
+// HD = 2 kHFixBits2; balanced base-256 digits hdig[(pos*HD + d)*R + r] and
+// the exponent hexp[pos*(R/64) + rb].
 template <int NG>
 __device__ __forceinline__ void write_h_digits(int R, int rb, int off, bool lead,
                                                const bool (&bv)[NG], const float (&hv)[NG][4],
                                                int8_t* __restrict__ hdig,
                                                int32_t* __restrict__ hexp,
                                                float (*bmax)[NG * kTokPerGroup]) {
+  constexpr int HD = h_digits(NG);
   const int nrb = R / kBlk;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kg = lane >> 4;
@@ -50,22 +54,30 @@ __device__ __forceinline__ void write_h_digits(int R, int rb, int off, bool lead
     if (!(lead && bv[cg])) continue;
     const int ti = cg * kTokPerGroup + m;
     const float mx = fmaxf(fmaxf(bmax[0][ti], bmax[1][ti]), fmaxf(bmax[2][ti], bmax[3][ti]));
-    const int Eh = kFixBits - exp_bound(mx);
+    const int Eh = (HD == 3 ? kFixBits : kHFixBits2) - exp_bound(mx);
     uint32_t w0 = 0, w1 = 0, w2 = 0;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
+      // |hv| <= mx < 2^exp_bound(mx): |v| <= 2^22 (2^14), so the top digit
+      // stays within [-64, 64]
       const int v = (int)rintf(ldexpf(hv[cg][i], Eh));
       int d0, d1, d2;
-      split_digits(v, d0, d1, d2);
+      if constexpr (HD == 3) {
+        split_digits(v, d0, d1, d2);
+      } else {
+        d0 = (int)(int8_t)(v & 0xFF);
+        d1 = (v - d0) >> 8;
+        d2 = 0;
+      }
       w0 |= (uint32_t)(d0 & 0xFF) << (8 * i);
       w1 |= (uint32_t)(d1 & 0xFF) << (8 * i);
       w2 |= (uint32_t)(d2 & 0xFF) << (8 * i);
     }
     const size_t pos = (size_t)off + ti;
-    int8_t* hp = hdig + pos * kDigits * R + rbase;
+    int8_t* hp = hdig + pos * HD * R + rbase;
     *(uint32_t*)(hp) = w0;
     *(uint32_t*)(hp + R) = w1;
-    *(uint32_t*)(hp + 2 * (size_t)R) = w2;
+    if constexpr (HD == 3) *(uint32_t*)(hp + 2 * (size_t)R) = w2;
     if (wave == 0 && kg == 0) hexp[pos * nrb + rb] = Eh;
   }
 }
@@ -76,8 +88,8 @@ __device__ __forceinline__ void write_h_digits(int R, int rb, int off, bool lead
 // r16%3; bv[cg] says whether that column holds a token and xev[cg] is the
 // token's fixed-point exponent.  load_b(cg, ks) returns this lane's 16 digit
 // bytes of k-step ks (k = 64*ks + 16*(lane/16) .. +15).  Writes H' of the
-// group's positions off .. off+n-1 as per-block fixed-point digits:
-// hdig[(pos*3 + d)*R + r], hexp[pos*(R/64) + rb].
+// group's positions off .. off+n-1 as per-block fixed-point digits
+// (write_h_digits).
 template <int NG, typename LoadB>
 __device__ __forceinline__ void gateup_block(int C, int R, int rb, const int8_t* __restrict__ blob,
                                              int off, const bool (&bv)[NG], const int (&xev)[NG],

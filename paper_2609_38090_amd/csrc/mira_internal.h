@@ -13,11 +13,18 @@ namespace mira {
 // ---------------------------------------------------------------------------
 // Compile-time tiling constants
 // ---------------------------------------------------------------------------
-constexpr int kDigits = 3;           // base-256 digits of a fixed-point activation
-constexpr int kFixBits = 22;         // |fixed-point value| < 2^22
+constexpr int kDigits = 3;           // base-256 digits of a fixed-point activation x
+constexpr int kFixBits = 22;         // |fixed-point x| < 2^22
 constexpr int kBlk = 64;             // rows of H' sharing one fixed-point exponent
-constexpr int kTokPerGroup = 5;      // tokens per 16-column MFMA operand (3 digits each)
+constexpr int kTokPerGroup = 5;      // tokens per 16-column MFMA operand of x (3 digits each)
 constexpr int kDecodeMaxGroups = (MIRA_DECODE_MAX_TOKENS + kTokPerGroup - 1) / kTokPerGroup;
+// H' (the down projection's input) is written as three digits (kFixBits) when
+// one x group covers the call (T <= kTokPerGroup) and as two digits of
+// kHFixBits2 bits otherwise, so that an operand of H' holds 8 tokens instead
+// of 5 and the down kernel needs half the token groups.
+constexpr int kHFixBits2 = 14;       // two digits: |fixed-point H'| <= 2^14 (digits stay in int8)
+__host__ __device__ constexpr int h_digits(int x_groups) { return x_groups == 1 ? 3 : 2; }
+__host__ __device__ constexpr int h_tok_per_group(int hd) { return hd == 3 ? 5 : 8; }
 constexpr int kPrefBM = 128;         // prefill tile: tokens per m-tile (shared by both GEMMs)
 
 inline __host__ __device__ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -119,7 +126,7 @@ inline Layout make_layout(const mira_shape& s, int T) {
   L.pcnt = take((size_t)kPermChunkMax * L.E * 4);
   L.dwork = take(G * sizeof(DecodeWork));
   L.xdig = take((size_t)L.Td * kDigits * L.C);
-  L.hdig = take((size_t)L.Pd * kDigits * L.R);
+  L.hdig = take((size_t)L.Pd * kDigits * L.R);  // room for three digits
   L.hexp = take((size_t)L.Pd * (L.R / kBlk) * 4);
   L.xb16 = take(s.act_dtype == MIRA_F32 ? Tz * L.C * 2 : 0);
   L.hbuf = take(P * L.R * 2);

@@ -18,6 +18,17 @@ FFN_MAX_ABS_RMS = 2e-2   # max-abs error bar, in units of rms(out)
 NEAR_TIE = 1e-4          # logit gap below which a top-k decision is ambiguous
 
 
+def decode_rel_floor(T):
+    """Relative Frobenius error the integer decode path keeps to, well inside
+    FFN_REL_FRO: the int8 matrix-core sums are exact and the rounding is the
+    fixed point of x (22 bits of the token's maximum) and of H' (22 bits of its
+    64-row block maximum up to 5 tokens; 14 bits above, where H' is carried as
+    two digits so an operand holds 8 tokens).  At 14 bits one H' entry is off
+    by at most 2^-14 of its block maximum; the outputs of these inputs then
+    differ by about 1e-4 of their norm."""
+    return 1e-4 if T <= 5 else 1e-3
+
+
 def act_dtype(cfg):
     return mira.MIRA_F32 if cfg.act == "f32" else mira.MIRA_BF16
 

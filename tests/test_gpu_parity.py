@@ -8,7 +8,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_layer import EPS, Layer, act_dtype, assert_ffn_close, run_and_check
+from gpu_layer import EPS, Layer, act_dtype, assert_ffn_close, decode_rel_floor, run_and_check
 from mira_inputs import CONFIGS, MoEConfig, predictor_weights, activations
 
 pytestmark = pytest.mark.gpu
@@ -45,9 +45,10 @@ def test_pack_bit_exact_bf16_input_and_padding(mira):
         assert not got[e, ref.size:].any()
 
 
-def test_tiny_decode_path(mira):
-    res, errs, _, _ = run_and_check(Layer(CONFIGS["tiny"]))
-    assert errs[0] < 1e-4  # the integer decode path is close to fp32-exact
+@pytest.mark.parametrize("T", [16, 5])
+def test_tiny_decode_path(mira, T):
+    res, errs, _, _ = run_and_check(Layer(CONFIGS["tiny"], T=T))
+    assert errs[0] < decode_rel_floor(T), errs  # the integer decode path keeps well inside the bar
 
 
 def test_tiny_prefill_path(mira):
