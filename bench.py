@@ -44,13 +44,13 @@ PROF_EVERY = 8  # steps timed with events: one layer-copy rotation in every 8
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 TRAFFIC = {
     ("decode_gateup", "mixtral_decode"): dict(sources=("decode.hip", "decode_dev.h", "int4_format.h"),
-                                               sha="7dea4bd328214dd8", fetch_kib=114822.7, write_kib=98.0),
+                                               sha="5d61aa99525b7b6e", fetch_kib=114816.7, write_kib=98.0),
     ("decode_gateup", "mixtral_decode_int4"): dict(sources=("decode.hip", "decode_dev.h", "int4_format.h"),
-                                                    sha="7dea4bd328214dd8", fetch_kib=61050.4, write_kib=98.0),
-    ("prefill_gateup", "mixtral_prefill"): dict(sources=("prefill.hip",), sha="a1fac0bd38061bf5",
-                                                 fetch_kib=599131.7, write_kib=37599.8),
-    ("prefill_gateup", "fine_grained"): dict(sources=("prefill.hip",), sha="a1fac0bd38061bf5",
-                                              fetch_kib=290115.5, write_kib=57402.6),
+                                                    sha="5d61aa99525b7b6e", fetch_kib=61055.8, write_kib=98.0),
+    ("prefill_gateup", "mixtral_prefill"): dict(sources=("prefill.hip",), sha="bbbf3d7834e0cc58",
+                                                 fetch_kib=600953.2, write_kib=37751.2),
+    ("prefill_gateup", "fine_grained"): dict(sources=("prefill.hip",), sha="bbbf3d7834e0cc58",
+                                              fetch_kib=290069.9, write_kib=57286.4),
 }
 
 
