@@ -119,4 +119,54 @@ __device__ __forceinline__ float head_col_sum(int rows, Load load) {
   return s;
 }
 
+// f[i][c] = (1/group) * sum over rows [i*group, (i+1)*group) of x[row][c],
+// i < n, written to LDS by one 256-thread workgroup: 16-byte loads of 8 rows
+// at a time, each column summed over its rows in order (the same arithmetic,
+// column by column, as head_col_sum).  C * sizeof(ActT) is a multiple of 16
+// and x is 16-byte aligned.  The caller synchronises before reading f.
+constexpr int kFusedPoolFloats = 16384;  // pooled rows kept in LDS: 64 KB
+
+template <typename ActT>
+__device__ __forceinline__ void head_pool_rows_lds(const ActT* __restrict__ x, int C, int n, int group,
+                                                   float* f) {
+  constexpr int VW = 16 / sizeof(ActT);  // columns per 16-byte load
+  const int nv = C / VW;
+  for (int q = threadIdx.x; q < n * nv; q += 256) {
+    const int i = q / nv, c = (q - i * nv) * VW;
+    float s[VW];
+#pragma unroll
+    for (int u = 0; u < VW; ++u) s[u] = 0.f;
+    for (int r = 0; r < group; r += 8) {
+      const int rn = min(8, group - r);
+      v4i v[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t)
+        v[t] = t < rn ? ld16(x + (size_t)(i * group + r + t) * C + c) : zero16();
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        if (t < rn) {
+#pragma unroll
+          for (int u = 0; u < VW; ++u) {
+            float a;
+            if constexpr (sizeof(ActT) == 2)
+              a = __uint_as_float(((uint32_t)v[t][u / 2] >> (16 * (u % 2))) << 16);
+            else
+              a = __int_as_float(v[t][u]);
+            s[u] += a;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < VW; ++u) f[(size_t)i * C + c + u] = s[u] / (float)group;
+  }
+}
+
+// Whether a call of n pooled rows of C activations at x may pool inside its
+// first layer's kernel (head_pool_rows_lds): few rows, 16-byte loads.
+inline bool head_fused_pool_ok(const void* x, int n, int C, size_t act_bytes, int max_groups) {
+  return n <= max_groups && (size_t)n * C <= (size_t)kFusedPoolFloats && (C * act_bytes) % 16 == 0 &&
+         (uintptr_t)x % 16 == 0;
+}
+
 }  // namespace mira

@@ -2,7 +2,8 @@
 // hidden row and the mean router logits, a HistHead over the selection
 // histogram and the top-m indicator, mixed by a contextual gate.  Three
 // kernels over all groups of a call: features, the hidden layers of both heads
-// plus the gate unit, then the output layers, the mix and the softmax.
+// plus the gate unit, then the output layers, the mix and the softmax; with
+// few groups the features are built inside the hidden layer's kernel.
 // fp32 accumulation throughout.
 #include "device_util.h"
 #include "head_dev.h"
@@ -35,6 +36,34 @@ MixWs mix_ws(void* ws, int n, int C, int E) {
   return w;
 }
 
+// Routing features of group i, by one 256-thread workgroup: fi[0..E) the
+// mean router logits, fi[E..2E) the selection histogram (share of the
+// group's pairs per expert), fi[2E..3E) the indicator of the m most selected
+// experts (ties to the lower index).  cnt is E ints of LDS.
+__device__ __forceinline__ void group_features(const float* __restrict__ logits,
+                                               const int32_t* __restrict__ topk_idx, int E, int k,
+                                               int m, int group, int i, int* cnt, float* fi) {
+  const int tid = threadIdx.x;
+  for (int e = tid; e < E; e += 256) cnt[e] = 0;
+  __syncthreads();
+  const int pairs = group * k;
+  const int32_t* ti = topk_idx + (size_t)i * pairs;
+  for (int p = tid; p < pairs; p += 256) {
+    const int e = ti[p];
+    if (e >= 0 && e < E) atomicAdd(&cnt[e], 1);
+  }
+  __syncthreads();
+  for (int e = tid; e < E; e += 256) {
+    const float s = head_col_sum(group, [&](int r) { return logits[(size_t)(i * group + r) * E + e]; });
+    const int c = cnt[e];
+    int rank = 0;  // experts ahead of e: more pairs, or as many and a lower index
+    for (int f = 0; f < E; ++f) rank += (cnt[f] > c) || (cnt[f] == c && f < e);
+    fi[e] = s / (float)group;
+    fi[E + e] = (float)c / (float)pairs;
+    fi[2 * E + e] = (rank < m && c > 0) ? 1.f : 0.f;
+  }
+}
+
 // Grid (C/256 + 1, n).  Blocks x < C/256 pool 256 hidden columns of group
 // blockIdx.y; the last block builds the routing features of that group.
 template <typename ActT>
@@ -54,38 +83,16 @@ __global__ __launch_bounds__(256) void mix_features_kernel(const ActT* __restric
     return;
   }
   __shared__ int cnt[MIRA_MAX_EXPERTS];
-  for (int e = tid; e < E; e += 256) cnt[e] = 0;
-  __syncthreads();
-  const int pairs = group * k;
-  const int32_t* ti = topk_idx + (size_t)i * pairs;
-  for (int p = tid; p < pairs; p += 256) {
-    const int e = ti[p];
-    if (e >= 0 && e < E) atomicAdd(&cnt[e], 1);
-  }
-  __syncthreads();
-  float* fi = feat + (size_t)i * 3 * E;
-  for (int e = tid; e < E; e += 256) {
-    const float s = head_col_sum(group, [&](int r) { return logits[(size_t)(i * group + r) * E + e]; });
-    const int c = cnt[e];
-    int rank = 0;  // experts ahead of e: more pairs, or as many and a lower index
-    for (int f = 0; f < E; ++f) rank += (cnt[f] > c) || (cnt[f] == c && f < e);
-    fi[e] = s / (float)group;
-    fi[E + e] = (float)c / (float)pairs;
-    fi[2 * E + e] = (rank < m && c > 0) ? 1.f : 0.f;
-  }
+  group_features(logits, topk_idx, E, k, m, group, i, cnt, feat + (size_t)i * 3 * E);
 }
 
-// One wave per row r of the stacked hidden layer: rows [0, Pa) are the
-// ActHead, [Pa, Pa+Ph) the HistHead, row Pa+Ph the gate unit.  Each wave
+// Row r of the stacked hidden layer, by one wave: rows [0, Pa) are the
+// ActHead, [Pa, Pa+Ph) the HistHead, row Pa+Ph the gate unit.  The wave
 // sweeps its weight row once per kMixGroups groups.
-__global__ __launch_bounds__(256) void mix_hidden_kernel(mira_mixture_weights w, int C, int E,
-                                                         int Pa, int Ph, int n,
-                                                         const float* __restrict__ h,
-                                                         const float* __restrict__ feat,
-                                                         float* __restrict__ z) {
-  const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+__device__ __forceinline__ void hidden_row(const mira_mixture_weights& w, int C, int E, int Pa, int Ph,
+                                           int n, const float* h, const float* feat,
+                                           float* __restrict__ z, int r, int lane) {
   const int rows = Pa + Ph + 1;
-  if (r >= rows) return;
   const uint16_t *wc = nullptr, *wl = nullptr, *wq = nullptr, *wu = nullptr;
   float bias = 0.f;
   bool relu = true;
@@ -125,6 +132,42 @@ __global__ __launch_bounds__(256) void mix_hidden_kernel(mira_mixture_weights w,
       }
     }
   }
+}
+
+// One wave per row of the stacked hidden layer (hidden_row).
+__global__ __launch_bounds__(256) void mix_hidden_kernel(mira_mixture_weights w, int C, int E,
+                                                         int Pa, int Ph, int n,
+                                                         const float* __restrict__ h,
+                                                         const float* __restrict__ feat,
+                                                         float* __restrict__ z) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (r >= Pa + Ph + 1) return;
+  hidden_row(w, C, E, Pa, Ph, n, h, feat, z, r, lane);
+}
+
+// Features and the hidden layer in one launch, for calls with few groups
+// (head_fused_pool_ok and the features in LDS): every workgroup pools the
+// hidden rows and builds the routing features of all groups in LDS itself,
+// with the arithmetic of the separate kernels, so the bits are the same.
+template <typename ActT>
+__global__ __launch_bounds__(256) void mix_fused_hidden_kernel(const ActT* __restrict__ x,
+                                                               const float* __restrict__ logits,
+                                                               const int32_t* __restrict__ topk_idx,
+                                                               mira_mixture_weights w, int C, int E,
+                                                               int k, int m, int group, int Pa, int Ph,
+                                                               int n, float* __restrict__ z) {
+  extern __shared__ __attribute__((aligned(16))) float sm[];  // [n][C] pooled, then [n][3][E]
+  __shared__ int cnt[MIRA_MAX_EXPERTS];
+  float* h_s = sm;
+  float* f_s = sm + (size_t)n * C;
+  head_pool_rows_lds(x, C, n, group, h_s);
+  for (int i = 0; i < n; ++i) {
+    group_features(logits, topk_idx, E, k, m, group, i, cnt, f_s + (size_t)i * 3 * E);
+    __syncthreads();  // cnt is reused by the next group
+  }
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (r >= Pa + Ph + 1) return;
+  hidden_row(w, C, E, Pa, Ph, n, h_s, f_s, z, r, lane);
 }
 
 // One block of 16 waves per group: a wave per output (both output layers'
@@ -184,15 +227,28 @@ hipError_t launch_mixture(const mira_mixture_shape& p, const mira_mixture_weight
   const int C = p.hidden, E = p.n_src, Pa = p.act_hidden, Ph = p.hist_hidden;
   const MixWs m = mix_ws(ws, n, C, E);
   prof_begin("mixture", st);
-  const dim3 gf((C + 255) / 256 + 1, n);
-  if (p.act_dtype == MIRA_BF16)
-    hipLaunchKernelGGL(mix_features_kernel<uint16_t>, gf, dim3(256), 0, st, (const uint16_t*)x,
-                       logits, topk_idx, C, E, p.top_k, p.hist_top, p.group, m.h, m.feat);
-  else
-    hipLaunchKernelGGL(mix_features_kernel<float>, gf, dim3(256), 0, st, (const float*)x, logits,
-                       topk_idx, C, E, p.top_k, p.hist_top, p.group, m.h, m.feat);
-  hipLaunchKernelGGL(mix_hidden_kernel, dim3((Pa + Ph + 1 + 3) / 4), dim3(256), 0, st, w, C, E, Pa,
-                     Ph, n, m.h, m.feat, m.z);
+  const size_t fused_floats = (size_t)n * C + (size_t)n * 3 * E;
+  if (head_fused_pool_ok(x, n, C, p.act_dtype == MIRA_BF16 ? 2 : 4, kMixGroups) &&
+      fused_floats <= (size_t)kFusedPoolFloats) {
+    const dim3 gh((Pa + Ph + 1 + 3) / 4);
+    const size_t lds = fused_floats * sizeof(float);
+    if (p.act_dtype == MIRA_BF16)
+      hipLaunchKernelGGL(mix_fused_hidden_kernel<uint16_t>, gh, dim3(256), lds, st, (const uint16_t*)x, logits,
+                         topk_idx, w, C, E, p.top_k, p.hist_top, p.group, Pa, Ph, n, m.z);
+    else
+      hipLaunchKernelGGL(mix_fused_hidden_kernel<float>, gh, dim3(256), lds, st, (const float*)x, logits,
+                         topk_idx, w, C, E, p.top_k, p.hist_top, p.group, Pa, Ph, n, m.z);
+  } else {
+    const dim3 gf((C + 255) / 256 + 1, n);
+    if (p.act_dtype == MIRA_BF16)
+      hipLaunchKernelGGL(mix_features_kernel<uint16_t>, gf, dim3(256), 0, st, (const uint16_t*)x,
+                         logits, topk_idx, C, E, p.top_k, p.hist_top, p.group, m.h, m.feat);
+    else
+      hipLaunchKernelGGL(mix_features_kernel<float>, gf, dim3(256), 0, st, (const float*)x, logits,
+                         topk_idx, C, E, p.top_k, p.hist_top, p.group, m.h, m.feat);
+    hipLaunchKernelGGL(mix_hidden_kernel, dim3((Pa + Ph + 1 + 3) / 4), dim3(256), 0, st, w, C, E, Pa,
+                       Ph, n, m.h, m.feat, m.z);
+  }
   hipLaunchKernelGGL(mix_out_kernel, dim3(n), dim3(kOutWaves * 64), 0, st, w, Pa, Ph, p.n_out, m.z, probs,
                      alpha);
   prof_end("mixture", st);

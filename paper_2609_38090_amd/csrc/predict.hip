@@ -1,6 +1,7 @@
 // Predictor head (paper section IV-E): mean-pool a group of token rows of
 // layer l's hidden states, then a two-layer MLP (ReLU, sigmoid) scoring the
-// experts of layer l+2.  Three small kernels, fp32 accumulation.
+// experts of layer l+2.  Three small kernels, fp32 accumulation; with few
+// pooled rows the pooling runs inside the first layer's kernel.
 #include "device_util.h"
 #include "head_dev.h"
 #include "mira_internal.h"
@@ -46,6 +47,35 @@ __global__ __launch_bounds__(256) void pred_layer1_kernel(const uint16_t* __rest
   }
 }
 
+// Pooling and the first layer in one launch, for calls with few pooled rows
+// (head_fused_pool_ok): every workgroup pools the n groups into LDS itself,
+// so no pooled rows travel through memory and no launch sits between the two
+// steps; the results are the same bits as the separate kernels'.
+template <typename ActT>
+__global__ __launch_bounds__(256) void pred_pool_layer1_kernel(const ActT* __restrict__ x,
+                                                               const uint16_t* __restrict__ w1,
+                                                               const float* __restrict__ b1, int C,
+                                                               int P, int n, int group,
+                                                               float* __restrict__ z) {
+  extern __shared__ __attribute__((aligned(16))) float f_s[];  // [n][C]
+  head_pool_rows_lds(x, C, n, group, f_s);
+  __syncthreads();
+  const int p = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (p >= P) return;
+  float acc[kPredGroups];
+#pragma unroll
+  for (int j = 0; j < kPredGroups; ++j) acc[j] = 0.f;
+  head_row_dot(w1 + (size_t)p * C, f_s, C, n, lane, acc);
+  const float bias = b1 ? b1[p] : 0.f;
+#pragma unroll
+  for (int j = 0; j < kPredGroups; ++j) {
+    if (j < n) {
+      const float s = wave_sum(acc[j]);
+      if (lane == 0) z[(size_t)j * P + p] = fmaxf(s + bias, 0.f);
+    }
+  }
+}
+
 // scores[i][e] = 1 / (1 + exp(-(sum_p W2[e][p] z[i][p] + b2[e]))); one wave per (i, e)
 __global__ __launch_bounds__(256) void pred_layer2_kernel(const uint16_t* __restrict__ w2,
                                                           const float* __restrict__ b2,
@@ -68,6 +98,20 @@ hipError_t launch_predict(const mira_pred_shape& p, const void* x, int T, const 
   float* f = (float*)ws;
   float* z = (float*)((char*)ws + align_up((size_t)n * p.hidden * 4, 256));
   prof_begin("predict", st);
+  if (head_fused_pool_ok(x, n, p.hidden, p.act_dtype == MIRA_BF16 ? 2 : 4, kPredGroups)) {
+    const size_t lds = (size_t)n * p.hidden * sizeof(float);
+    if (p.act_dtype == MIRA_BF16)
+      hipLaunchKernelGGL(pred_pool_layer1_kernel<uint16_t>, dim3((p.pred_hidden + 3) / 4), dim3(256), lds,
+                         st, (const uint16_t*)x, (const uint16_t*)w1, b1, p.hidden, p.pred_hidden, n,
+                         p.group, z);
+    else
+      hipLaunchKernelGGL(pred_pool_layer1_kernel<float>, dim3((p.pred_hidden + 3) / 4), dim3(256), lds, st,
+                         (const float*)x, (const uint16_t*)w1, b1, p.hidden, p.pred_hidden, n, p.group, z);
+    hipLaunchKernelGGL(pred_layer2_kernel, dim3((n * p.n_out + 3) / 4), dim3(256), 0, st,
+                       (const uint16_t*)w2, b2, z, p.pred_hidden, p.n_out, n, scores);
+    prof_end("predict", st);
+    return hipGetLastError();
+  }
   dim3 gpool((p.hidden + 255) / 256, n);
   if (p.act_dtype == MIRA_BF16)
     hipLaunchKernelGGL(pred_pool_kernel<uint16_t>, gpool, dim3(256), 0, st, (const uint16_t*)x,

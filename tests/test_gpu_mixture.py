@@ -120,3 +120,35 @@ def test_mixture_head_histogram_branch_alone(mira):
     assert np.array_equal(np.argsort(-probs.cpu().numpy(), axis=1, kind="stable")[:, :2],
                           np.argsort(-ref["probs"], axis=1, kind="stable")[:, :2])
 
+
+
+def test_mixture_head_groups_are_independent(mira):
+    """A group's prediction does not depend on the other groups of the call:
+    1 and 4 groups (features built inside the hidden layer's kernel) and 5
+    groups (separate features kernel) give the same bits for the groups they
+    share, and match the oracle."""
+    name, cid, C, E, k, m, Pa, Ph, N, group, T, act = CASES[2]  # the beam shape
+    cfg = MoEConfig(name, cid, T=40, C=C, E=E, k=k, R=64, act=act, zipf_s=1.1)
+    x = activations(cfg, 0, "cpu")
+    logits, idx = routing_sample(cfg, 0)
+    W = mixture_weights(cfg, 0, Pa, Ph, N)
+    shape = mira.MixtureShape(C, E, k, m, Pa, Ph, N, group, mira.MIRA_BF16)
+    w = mira.MixtureWeights(**{key: v.cuda() for key, v in W.items() if torch.is_tensor(v)}, bg=W["bg"])
+    xd, ld, id_ = x.cuda(), logits.cuda(), idx.cuda()
+    out = {}
+    for t in (40, 32, 8):
+        n = t // group
+        ws = torch.full((max(256, mira.mira_mixture_workspace_bytes(shape, t)),), 0xFF, dtype=torch.uint8,
+                        device="cuda")
+        probs = torch.empty((n, N), dtype=torch.float32, device="cuda")
+        alpha = torch.empty((n,), dtype=torch.float32, device="cuda")
+        mira.mira_predict_mixture(shape, w, xd[:t], ld[:t], id_[:t], t, probs, alpha, ws, ws.numel())
+        torch.cuda.synchronize()
+        out[t] = (probs.cpu().numpy(), alpha.cpu().numpy())
+    for t in (32, 8):
+        n = t // group
+        assert np.array_equal(out[t][0], out[40][0][:n]), t
+        assert np.array_equal(out[t][1], out[40][1][:n]), t
+    W64 = {key: (v.double().numpy() if torch.is_tensor(v) else v) for key, v in W.items()}
+    ref = oracle.mixture_head(x.double().numpy(), logits.double().numpy(), idx.numpy(), group, m, W64)
+    assert np.allclose(out[40][0], ref["probs"], rtol=1e-4, atol=1e-7)

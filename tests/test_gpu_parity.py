@@ -319,7 +319,9 @@ def test_predictor_groups_are_independent(mira):
     """A group's scores do not depend on the other groups of the call (1, 4
     or 5 groups give bit-identical scores for the groups they share), from a
     workspace of 0xFF bytes and when the workspace is reused; all match the
-    oracle."""
+    oracle.  Calls of up to 4 groups pool inside the first layer's kernel and
+    5 groups take the separate pooling kernel, so this also checks that both
+    give the same bits."""
     cfg = CONFIGS["beam_stack"]
     x = activations(cfg, 4, "cpu", T=40)
     w1, b1, w2, b2 = predictor_weights(cfg, 4, "cpu")
