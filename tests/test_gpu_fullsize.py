@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_layer import EPS, LazyBlobs, Layer, run_and_check
+from gpu_layer import EPS, LazyBlobs, Layer, decode_rel_floor, run_and_check
 from mira_inputs import CONFIGS, activations, predictor_weights
 import oracle
 
@@ -28,6 +28,19 @@ def test_mixtral_decode_layer(mira):
     _check_packed(lay, blobs)
     assert len(blobs.cache) == 2
     print(f"mixtral decode: rel_fro={errs[0]:.2e} max_abs/rms={errs[1]:.2e}")
+
+
+# The decode path at the other full-size shapes: 16 Mixtral tokens (four
+# x groups, H' as two digits in two groups of 8) and the fine-grained layer
+# (64 routed experts, top-6, 2 shared) at 1 and 16 tokens.
+@pytest.mark.parametrize("name,T", [("mixtral_decode", 16), ("fine_grained", 1), ("fine_grained", 16)])
+def test_full_size_decode_shapes(mira, name, T):
+    lay = Layer(CONFIGS[name], T=T)
+    assert T <= mira.MIRA_DECODE_MAX_TOKENS
+    res, errs, blobs, ties = run_and_check(lay)
+    _check_packed(lay, blobs)
+    assert errs[0] < decode_rel_floor(T), errs
+    print(f"{name} decode T={T}: rel_fro={errs[0]:.2e} max_abs/rms={errs[1]:.2e} near-ties={len(ties)}")
 
 
 class _Run:
