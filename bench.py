@@ -44,24 +44,34 @@ PROF_EVERY = 8  # steps timed with events: one layer-copy rotation in every 8
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 TRAFFIC = {
     ("decode_gateup", "mixtral_decode"): dict(sources=("decode.hip", "decode_dev.h", "int4_format.h"),
-                                               sha="5d61aa99525b7b6e", fetch_kib=114816.7, write_kib=98.0),
+                                               sha="799cc7d8a425d2ac", fetch_kib=114816.7, write_kib=98.0),
     ("decode_gateup", "mixtral_decode_int4"): dict(sources=("decode.hip", "decode_dev.h", "int4_format.h"),
-                                                    sha="5d61aa99525b7b6e", fetch_kib=61055.8, write_kib=98.0),
-    ("prefill_gateup", "mixtral_prefill"): dict(sources=("prefill.hip",), sha="bbbf3d7834e0cc58",
+                                                    sha="799cc7d8a425d2ac", fetch_kib=61055.8, write_kib=98.0),
+    ("prefill_gateup", "mixtral_prefill"): dict(sources=("prefill.hip",), sha="66936ada042c71be",
                                                  fetch_kib=600953.2, write_kib=37751.2),
-    ("prefill_gateup", "fine_grained"): dict(sources=("prefill.hip",), sha="bbbf3d7834e0cc58",
+    ("prefill_gateup", "fine_grained"): dict(sources=("prefill.hip",), sha="66936ada042c71be",
                                               fetch_kib=290069.9, write_kib=57286.4),
 }
 
 
+def strip_comments(text):
+    """C/C++ source without its comments and blank space, so that only code
+    changes alter a source hash (string literals are kept as they are)."""
+    import re
+    pat = re.compile(r'//[^\n]*|/\*.*?\*/|"(?:\\.|[^"\\])*"', re.S)
+    code = pat.sub(lambda m: m.group(0) if m.group(0).startswith('"') else " ", text)
+    return " ".join(code.split())
+
+
 def source_hash(sources):
-    """Hash of the kernel sources and the two shared headers."""
+    """Hash of the code (comments and spacing dropped) of the kernel sources
+    and the two shared headers."""
     import hashlib
     csrc = os.path.join(ROOT, "paper_2609_38090_amd", "csrc")
     h = hashlib.sha256()
     for f in tuple(sources) + ("device_util.h", "mira_internal.h"):
-        with open(os.path.join(csrc, f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(csrc, f), encoding="utf-8") as fh:
+            h.update(strip_comments(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -215,7 +215,16 @@ size_t mira_workspace_bytes(const mira_shape* s, int32_t max_tokens);
  * pairs by expert, SwiGLU expert FFN on the packed experts fetched through
  * slot_table, weighted combine into out.  Reads status-free inputs only;
  * writes out and the optional outputs.  Deterministic: repeated calls on the
- * same inputs give bit-identical results. */
+ * same inputs give bit-identical results.
+ * Arithmetic: with n_tokens <= MIRA_DECODE_MAX_TOKENS (or MIRA_FLAG_FORCE_DECODE)
+ * the experts run on int8 matrix cores with the packed bytes as one operand
+ * and the activations as fixed-point digits as the other, so the sums are
+ * exact integers and the rounding is that of the fixed points: x at 2^-22 of
+ * each token's maximum, H' at 2^-22 of the maximum of its 64-row block when
+ * the call has at most 5 tokens and 2^-14 above.  Otherwise (or with
+ * MIRA_FLAG_FORCE_PREFILL) the int8 weights are widened exactly to bf16 for
+ * bf16 matrix cores with fp32 accumulation, x is rounded to bf16 when it is
+ * fp32, and H' is held in bf16.  Both paths take the same routing. */
 int mira_moe_forward(const mira_shape* s, const mira_moe_args* a, hipStream_t stream);
 
 /* The same call split in two so a runtime can fetch missing experts in

@@ -4,11 +4,13 @@
 // With one to a few tokens per expert the step is bound by streaming the
 // packed int8 bytes from HBM.  Both kernels feed those bytes unchanged to the
 // int8 matrix cores (v_mfma_i32_16x16x64_i8): the activation side is written
-// as a fixed-point integer split into three signed base-256 digits, each digit
-// one int8 operand column, so the products and sums are exact int32 and the
-// only rounding is the fixed-point step (relative 2^-22 of the row or block
-// maximum) and the final fp32 arithmetic.  Since the shared scale sigma_r
-// factors out (section IV-B), y = Qd H' with H' = sigma (.) silu(G) (.) U.
+// as a fixed-point integer split into signed base-256 digits, each digit one
+// int8 operand column, so the products and sums are exact int32 and the only
+// rounding is the fixed-point step and the final fp32 arithmetic.  x has three
+// digits (2^-22 of the token's maximum); H' three (2^-22 of its 64-row block
+// maximum) when the call has at most 5 tokens, else two (2^-14).  Since the
+// shared scale sigma_r factors out (section IV-B), y = Qd H' with
+// H' = sigma (.) silu(G) (.) U.
 #include "decode_dev.h"
 
 namespace mira {
