@@ -39,8 +39,9 @@ PROF_EVERY = 8  # steps timed with events: one layer-copy rotation in every 8
 # workload, each scaled by what the same counter reads for a plain 1 GiB
 # device copy (bench.py --copy-bytes 1073741824 reads FETCH_SIZE 524302 KiB
 # and WRITE_SIZE 1048576 KiB: scale 2.0 and 1.0).  An entry holds only for
-# the kernel sources it was measured on (hash of the kernel file and the two
-# shared headers); otherwise the bench reports traffic as null.
+# the kernel code it was measured on (hash of the kernel file and the two
+# shared headers with comments and spacing dropped); otherwise the bench
+# reports traffic as null.
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 TRAFFIC = {
     ("decode_gateup", "mixtral_decode"): dict(sources=("decode.hip", "decode_dev.h", "int4_format.h"),
