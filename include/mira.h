@@ -482,9 +482,12 @@ int mira_stack_destroy(mira_stack* st);
  * of page-locked host memory holding the packed expert. */
 int mira_stack_set_host(mira_stack* st, int32_t layer, int32_t expert, const void* pinned,
                         uint64_t bytes);
-/* Make HOT slot `slot` (< n_hot) hold expert e of layer l.  With copy = 1 the
- * expert's CPU-store blob is copied in (copy stream); with copy = 0 the
- * caller has written the slot's bytes already. */
+/* Make HOT slot `slot` hold expert e of layer l.  The HOT slots are the
+ * first n_hot slots of the pool until a rebalancing swap relabels a STAGE
+ * slot HOT and the victim's slot STAGE; a slot that is not HOT at the call is
+ * rejected (MIRA_ERR_ARG).  With copy = 1 the expert's CPU-store blob is
+ * copied in (copy stream); with copy = 0 the caller has written the slot's
+ * bytes already. */
 int mira_stack_set_hot(mira_stack* st, int32_t layer, int32_t expert, int32_t slot, int32_t copy);
 
 int mira_stack_begin_step(mira_stack* st);
@@ -492,7 +495,9 @@ int mira_stack_begin_step(mira_stack* st);
  * workspace; its slot_table, slot_pool, n_slots and slot_stride are taken
  * from the stack, and a NULL expert_counts is replaced by the stack's own
  * buffer.  head (may be NULL = MIRA_HEAD_NONE) picks layer l + lookahead's
- * experts to stage. */
+ * experts to stage.  An error after step 1 leaves part of the layer's work
+ * queued (copies issued, counters updated): end the step, call
+ * mira_stack_reset_stage and start a new step. */
 int mira_stack_layer(mira_stack* st, int32_t layer, const mira_moe_args* a,
                      const mira_stack_head* head);
 /* Wait for the step's work and add its counters (times included) to *stats

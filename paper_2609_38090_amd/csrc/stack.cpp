@@ -452,7 +452,9 @@ int mira_stack_set_hot(mira_stack* st, int32_t layer, int32_t expert, int32_t sl
   if (!st) return set_error(MIRA_ERR_ARG, "stack is NULL");
   if (layer < 0 || layer >= st->cfg.n_layers || expert < 0 || expert >= st->G)
     return set_error(MIRA_ERR_ARG, "layer or expert out of range");
-  if (slot < 0 || slot >= st->cfg.n_hot) return set_error(MIRA_ERR_ARG, "slot %d is not a HOT slot", slot);
+  // the HOT region is the first n_hot slots until rebalancing relabels slots
+  if (slot < 0 || slot >= st->n_slots || st->slots[slot].role != ROLE_HOT)
+    return set_error(MIRA_ERR_ARG, "slot %d is not a HOT slot", slot);
   Slot& s = st->slots[slot];
   if (s.layer >= 0 && s.expert >= 0 && st->hot[s.layer][s.expert] == slot) st->hot[s.layer][s.expert] = -1;
   if (st->hot[layer][expert] >= 0) st->slots[st->hot[layer][expert]].layer = -1;

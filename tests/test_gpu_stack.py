@@ -148,6 +148,7 @@ def test_rebalancer_tracks_drift_without_changing_outputs(mira):
                           rebalancer=Rebalancer(RebalanceConfig(interval=32, max_swaps=1, probation=2)))
     swaps = 0
     kinds = set()
+    log = []
     for s in range(24):
         ep = s // 6
         for st in (fixed, moving):
@@ -157,7 +158,9 @@ def test_rebalancer_tracks_drift_without_changing_outputs(mira):
         a, _ = run(fixed, "demand")
         b, stats = run(moving, "demand" if s % 2 else "predict")
         swaps += stats.swaps
-        kinds |= {ev[0] for ev in moving.events()}
+        evs = moving.events()
+        log += evs
+        kinds |= {ev[0] for ev in evs}
         for l in range(cfg.layers):
             assert np.array_equal(a[l], b[l]), (s, l)
         if s in (11, 23):  # after swaps: the rebalanced stack against the oracle
@@ -170,6 +173,17 @@ def test_rebalancer_tracks_drift_without_changing_outputs(mira):
     got_fixed = sum(len(fixed.hot_set(l) & last[l]) for l in range(cfg.layers))
     got_moving = sum(len(moving.hot_set(l) & last[l]) for l in range(cfg.layers))
     assert got_moving > got_fixed, (got_moving, got_fixed)
+    # HOT is a role that relabelling moves between slots: mira_stack_set_hot
+    # takes exactly the slots that are HOT now, whatever their index
+    hot_now = {slot: (l, e) for l in range(cfg.layers) for e, slot in moving.hot_slot[l].items()}
+    assert any(ev[0] == "swap_relabel" for ev in log)
+    assert len(hot_now) == moving.n_hot and set(hot_now) != set(range(moving.n_hot))
+    for slot in range(moving.n_slots):
+        if slot in hot_now:
+            mira.mira_stack_set_hot(moving.handle, *hot_now[slot], slot, copy=False)
+        else:
+            with pytest.raises(mira.MiraError):
+                mira.mira_stack_set_hot(moving.handle, 0, 0, slot, copy=False)
 
 
 def test_stack_with_mixture_head_stages_its_top_experts(mira):
