@@ -147,7 +147,7 @@ int run_route(const mira_shape* s, const mira_moe_args* a, const mira::Layout& L
     return MIRA_OK;
   }
   HIP_TRY(mira::launch_route(*s, L, w, a->x, a->w_router, a->router_bias, a->logits, st));
-  HIP_TRY(mira::launch_permute(*s, L, w, pool_of(a), a->expert_counts, a->topk_idx,
+  HIP_TRY(mira::launch_permute(L, w, pool_of(a), a->expert_counts, a->topk_idx,
                                a->topk_weight, a->expert_offsets, a->pair_order, st));
   return MIRA_OK;
 }
@@ -336,7 +336,7 @@ void prof_begin(const char* name, hipStream_t st) {
   if (!g_prof_on) return;
   if (!g_prof_only.empty() && g_prof_only != name) return;
   ProfRec r{name, prof_event(), nullptr};
-  if (r.a) hipEventRecord(r.a, st);
+  if (r.a) (void)hipEventRecord(r.a, st);  // timing only: a failed record drops the sample
   g_prof.push_back(r);
 }
 
@@ -358,7 +358,7 @@ void prof_end(const char* name, hipStream_t st) {
   for (auto it = g_prof.rbegin(); it != g_prof.rend(); ++it) {
     if (it->b == nullptr && std::strcmp(it->name, name) == 0) {
       it->b = prof_event();
-      if (it->b) hipEventRecord(it->b, st);
+      if (it->b) (void)hipEventRecord(it->b, st);
       return;
     }
   }

@@ -215,7 +215,7 @@ inline void launch_timed(const char* name, F kernel, dim3 grid, dim3 block, uint
 
 hipError_t launch_route(const mira_shape& s, const Layout& L, const WsPtr& w, const void* x,
                         const void* wr, const float* bias, float* logits_out, hipStream_t st);
-hipError_t launch_permute(const mira_shape& s, const Layout& L, const WsPtr& w,
+hipError_t launch_permute(const Layout& L, const WsPtr& w,
                           const ExpertPool& ep, int32_t* counts_out, int32_t* idx_out,
                           float* wts_out, int32_t* offsets_out, int32_t* order_out,
                           hipStream_t st);

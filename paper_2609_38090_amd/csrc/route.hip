@@ -535,7 +535,7 @@ hipError_t launch_route(const mira_shape& s, const Layout& L, const WsPtr& w, co
   return hipGetLastError();
 }
 
-hipError_t launch_permute(const mira_shape& s, const Layout& L, const WsPtr& w,
+hipError_t launch_permute(const Layout& L, const WsPtr& w,
                           const ExpertPool& ep, int32_t* counts_out, int32_t* idx_out,
                           float* wts_out, int32_t* offsets_out, int32_t* order_out,
                           hipStream_t st) {

@@ -408,31 +408,32 @@ int mira_stack_create(const mira_stack_config* cfg, const mira_shape* s, void* s
 
 int mira_stack_destroy(mira_stack* st) {
   if (!st) return mira::clear_error();
-  // let queued work that uses the stack's buffers finish first
-  if (st->copy) hipStreamSynchronize(st->copy);
-  if (st->side) hipStreamSynchronize(st->side);
-  if (st->compute) hipStreamSynchronize(st->compute);
+  // let queued work that uses the stack's buffers finish first; teardown
+  // goes on whatever these calls return
+  if (st->copy) (void)hipStreamSynchronize(st->copy);
+  if (st->side) (void)hipStreamSynchronize(st->side);
+  if (st->compute) (void)hipStreamSynchronize(st->compute);
   for (auto& s : st->slots)
-    if (s.copied) hipEventDestroy(s.copied);
+    if (s.copied) (void)hipEventDestroy(s.copied);
   for (auto ev : st->layer_done)
-    if (ev) hipEventDestroy(ev);
+    if (ev) (void)hipEventDestroy(ev);
   for (hipEvent_t ev : {st->ev_counts, st->ev_routed, st->ev_scores, st->wall0, st->wall1})
-    if (ev) hipEventDestroy(ev);
+    if (ev) (void)hipEventDestroy(ev);
   for (auto& p : st->copy_ev) {
-    hipEventDestroy(p.first);
-    hipEventDestroy(p.second);
+    (void)hipEventDestroy(p.first);
+    (void)hipEventDestroy(p.second);
   }
   for (auto& p : st->stall_ev) {
-    hipEventDestroy(p.first);
-    hipEventDestroy(p.second);
+    (void)hipEventDestroy(p.first);
+    (void)hipEventDestroy(p.second);
   }
-  for (auto ev : st->ev_pool) hipEventDestroy(ev);
-  if (st->counts_d) hipFree(st->counts_d);
-  if (st->counts_h) hipHostFree(st->counts_h);
-  if (st->scores_d) hipFree(st->scores_d);
-  if (st->scores_h) hipHostFree(st->scores_h);
-  if (st->copy) hipStreamDestroy(st->copy);
-  if (st->side) hipStreamDestroy(st->side);
+  for (auto ev : st->ev_pool) (void)hipEventDestroy(ev);
+  if (st->counts_d) (void)hipFree(st->counts_d);
+  if (st->counts_h) (void)hipHostFree(st->counts_h);
+  if (st->scores_d) (void)hipFree(st->scores_d);
+  if (st->scores_h) (void)hipHostFree(st->scores_h);
+  if (st->copy) (void)hipStreamDestroy(st->copy);
+  if (st->side) (void)hipStreamDestroy(st->side);
   delete st;
   return mira::clear_error();
 }
