@@ -275,3 +275,38 @@ def test_noalloc_forward_argument_checks():
         mira.mira_moe_forward_noalloc(s, a, stream=1)
     assert e.value.code == -4 and "MIRA_NOALLOC_SCRATCH_BYTES" in mira.mira_last_error()
     assert mira.mira_workspace_bytes(s, 16) <= mira.MIRA_NOALLOC_SCRATCH_BYTES
+
+
+def _stack_cfg(**kw):
+    C, R = 256, 512
+    base = dict(n_layers=4, n_hot=8, n_stage=4, max_tokens=8, slot_stride=mira.mira_packed_expert_bytes(C, R))
+    base.update(kw)
+    return mira.stack_config(**base), mira.MoEShape(C, R, 4, 2, 0, mira.MIRA_BF16)
+
+
+@pytest.mark.parametrize("change,code", [
+    (dict(n_layers=0), -2), (dict(n_hot=0, n_stage=0), -2), (dict(n_hot=-1), -2), (dict(max_tokens=0), -2),
+    (dict(vram_mode=7), -1), (dict(lookahead=0), -1), (dict(stage_per_layer=0), -1),
+    (dict(rb_interval=-1), -1), (dict(rb_interval=32, rb_probation=0), -1),
+    (dict(slot_stride=1000), -2), (dict(slot_stride=256), -2),
+])
+def test_stack_create_rejects_bad_settings_before_the_gpu(change, code):
+    """mira_stack_create checks its settings before any HIP call (these run
+    without a GPU)."""
+    cfg, shape = _stack_cfg(**change)
+    with pytest.raises(mira.MiraError) as e:
+        mira.mira_stack_create(cfg, shape, 0x100000, 0x2000, compute=1)
+    assert e.value.code == code, mira.mira_last_error()
+
+
+def test_stack_create_rejects_bad_shapes_and_pointers():
+    cfg, shape = _stack_cfg()
+    with pytest.raises(mira.MiraError) as e:
+        mira.mira_stack_create(cfg, mira.MoEShape(256, 512, 255, 2, 2, mira.MIRA_BF16), 0x100000, 0x2000, compute=1)
+    assert e.value.code == -2  # more than MIRA_MAX_EXPERTS experts per layer
+    with pytest.raises(mira.MiraError) as e:
+        mira.mira_stack_create(cfg, shape, None, 0x2000, compute=1)
+    assert e.value.code == -1
+    with pytest.raises(mira.MiraError) as e:
+        mira.mira_stack_create(cfg, shape, 0x100080, 0x2000, compute=1)
+    assert e.value.code == -3  # the slot pool must be 256-byte aligned

@@ -84,3 +84,13 @@ def test_more_than_one_gpu_is_refused():
     assert r.returncode == 2
     line = json.loads(r.stdout.strip().splitlines()[-1])
     assert "one GPU" in line["error"] and line["n_gpus"] == 2
+
+
+def test_source_hash_ignores_comments_but_not_code():
+    a = "int f(int x) { return x + 1; }  // one\n/* two\n   lines */\n"
+    b = "// another comment\nint   f(int x)\n{ return x + 1; }\n"
+    c = "int f(int x) { return x + 2; }\n"
+    d = 'const char* s = "// kept";\n'
+    assert bench.strip_comments(a) == bench.strip_comments(b)
+    assert bench.strip_comments(a) != bench.strip_comments(c)
+    assert "// kept" in bench.strip_comments(d)
