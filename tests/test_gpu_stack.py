@@ -32,7 +32,7 @@ def _head(mira, cfg, l, head):
 
 
 def build(mira, cfg, n_stage, hot=None, bias=None, host_all=False, rebalancer=None, head="mlp",
-          fmt="int8", vram_mode="large"):
+          fmt="int8", vram_mode="large", **stack_kw):
     from paper_2609_38090_amd.stack import ExpertStack, LayerData
     i4 = fmt == "int4"
     flag = mira.MIRA_FLAG_INT4 if i4 else 0
@@ -48,7 +48,7 @@ def build(mira, cfg, n_stage, hot=None, bias=None, host_all=False, rebalancer=No
     ps = (mira.PredShape(cfg.C, cfg.pred_hidden, cfg.E, cfg.pred_group, mira.MIRA_BF16) if head == "mlp" else
           mira.MixtureShape(cfg.C, cfg.E, cfg.k, cfg.k, MIX_PA, MIX_PH, cfg.E, cfg.pred_group, mira.MIRA_BF16))
     st = ExpertStack(shape, cfg.T, layers, stride, n_stage=n_stage, pred_shape=ps, rebalancer=rebalancer,
-                     vram_mode=vram_mode)
+                     vram_mode=vram_mode, **stack_kw)
     pack_shape = mira.MoEShape(cfg.C, cfg.R, 1, 1, flags=flag)
     hot_slot = st.hot_slot
     for l, ld in enumerate(layers):
