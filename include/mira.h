@@ -223,8 +223,11 @@ size_t mira_workspace_bytes(const mira_shape* s, int32_t max_tokens);
  * each token's maximum, H' at 2^-22 of the maximum of its 64-row block when
  * the call has at most 5 tokens and 2^-14 above.  Otherwise (or with
  * MIRA_FLAG_FORCE_PREFILL) the int8 weights are widened exactly to bf16 for
- * bf16 matrix cores with fp32 accumulation, x is rounded to bf16 when it is
- * fp32, and H' is held in bf16.  Both paths take the same routing. */
+ * bf16 matrix cores with fp32 accumulation and H' is held in bf16; with fp32
+ * activations x and H' are each carried as a high and a low bf16 part and
+ * both GEMMs run their contraction over both parts (twice the matrix work),
+ * so the result is near fp32 rather than bf16 accuracy.  Both paths take the
+ * same routing. */
 int mira_moe_forward(const mira_shape* s, const mira_moe_args* a, hipStream_t stream);
 
 /* The same call split in two so a runtime can fetch missing experts in

@@ -51,7 +51,7 @@ struct Layout {
   int mt_max;   // upper bound of prefill m-tiles
   int ksplit;   // most k-chunks of the prefill down GEMM (partials summed in order by the combine)
   size_t logits, idx, wts, counts, offsets, inv, tokpos, wpos, misc, active, mstart, pcnt,
-      dwork, xdig, hdig, hexp, xb16, hbuf, ybuf, total;
+      dwork, xdig, hdig, hexp, xb16, xlo16, hbuf, hlo, ybuf, total;
 };
 
 // One non-empty expert group of a decode call, written by the decode
@@ -128,8 +128,12 @@ inline Layout make_layout(const mira_shape& s, int T) {
   L.xdig = take((size_t)L.Td * kDigits * L.C);
   L.hdig = take((size_t)L.Pd * kDigits * L.R);  // room for three digits
   L.hexp = take((size_t)L.Pd * (L.R / kBlk) * 4);
-  L.xb16 = take(s.act_dtype == MIRA_F32 ? Tz * L.C * 2 : 0);
+  // fp32 activations: x and H' as high and low bf16 parts (two-pass GEMMs)
+  const bool f32 = s.act_dtype == MIRA_F32;
+  L.xb16 = take(f32 ? Tz * L.C * 2 : 0);
+  L.xlo16 = take(f32 ? Tz * L.C * 2 : 0);
   L.hbuf = take(P * L.R * 2);
+  L.hlo = take(f32 ? P * L.R * 2 : 0);
   L.ybuf = take((size_t)L.ksplit * P * L.C * 4);
   L.total = o;
   return L;
@@ -154,7 +158,9 @@ struct WsPtr {
   int8_t* hdig;
   int32_t* hexp;
   uint16_t* xb16;
+  uint16_t* xlo16;
   uint16_t* hbuf;
+  uint16_t* hlo;
   float* ybuf;
 };
 
@@ -178,7 +184,9 @@ inline WsPtr ws_ptrs(const Layout& L, void* base) {
   w.hdig = (int8_t*)(b + L.hdig);
   w.hexp = (int32_t*)(b + L.hexp);
   w.xb16 = (uint16_t*)(b + L.xb16);
+  w.xlo16 = (uint16_t*)(b + L.xlo16);
   w.hbuf = (uint16_t*)(b + L.hbuf);
+  w.hlo = (uint16_t*)(b + L.hlo);
   w.ybuf = (float*)(b + L.ybuf);
   return w;
 }

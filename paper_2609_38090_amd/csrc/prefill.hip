@@ -691,7 +691,7 @@ template <bool DUAL, int MS>
 __device__ __forceinline__ void tile_epilogue(const v4f (&acc)[kWaveTiles][MS], int wave,
                                               int lane, int n0, int N, int R, int C, int p0,
                                               int nv, const int8_t* blob, uint16_t* hout,
-                                              float* ybase) {
+                                              uint16_t* hout_lo, float* ybase) {
   const int r16 = lane & 15, kg = lane >> 4;
   // acc[j][ms][i] = weight row (tile base) + 4*kg + i, token p0 + ms*16 + r16
   if constexpr (DUAL) {
@@ -712,17 +712,24 @@ __device__ __forceinline__ void tile_epilogue(const v4f (&acc)[kWaveTiles][MS], 
       for (int ms = 0; ms < MS; ++ms) {
         const int tok = ms * 16 + r16;
         if (tok >= nv) continue;
-        uint32_t hb[4];
+        uint32_t hb[4], hl[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const float gv = sg[i] * acc[j][ms][i];
           const float uv = sg[i] * acc[4 + j][ms][i];
-          hb[i] = f32_to_bf16_rne(sg[i] * silu_mul(gv, uv));
+          const float h = sg[i] * silu_mul(gv, uv);
+          hb[i] = f32_to_bf16_rne(h);
+          hl[i] = f32_to_bf16_rne(h - __uint_as_float(hb[i] << 16));  // the rest, for two-pass calls
         }
         uint2 pk;
         pk.x = hb[0] | (hb[1] << 16);
         pk.y = hb[2] | (hb[3] << 16);
         *(uint2*)(hout + (size_t)(p0 + tok) * R + rr) = pk;
+        if (hout_lo) {
+          pk.x = hl[0] | (hl[1] << 16);
+          pk.y = hl[2] | (hl[3] << 16);
+          *(uint2*)(hout_lo + (size_t)(p0 + tok) * R + rr) = pk;
+        }
       }
     }
   } else {
@@ -740,12 +747,18 @@ __device__ __forceinline__ void tile_epilogue(const v4f (&acc)[kWaveTiles][MS], 
   }
 }
 
+// act_lo (may be null): the low bf16 parts of the activations (act holds
+// the high parts, act + act_lo the fp32 values to about 2^-16); with it every
+// tile runs its k range twice, over act and then over act_lo with the same
+// weights, into the same accumulators.  hout_lo (gate/up, may be null)
+// receives the low bf16 parts of H' for the down GEMM's second pass.
 template <bool DUAL>
 __global__ __launch_bounds__(kGemmThreads) void prefill_gemm_kernel(
     int C, int R, int G, int KSmax, ExpertPool ep, int32_t* __restrict__ misc,
     const int32_t* __restrict__ offsets,
     const int32_t* __restrict__ tokpos, const uint16_t* __restrict__ act,
-    uint16_t* __restrict__ hout, float* __restrict__ yout, size_t ysplit) {
+    const uint16_t* __restrict__ act_lo, uint16_t* __restrict__ hout,
+    uint16_t* __restrict__ hout_lo, float* __restrict__ yout, size_t ysplit) {
   // LDS ring of three 48 KB slots: 32 packed tiles exactly as in HBM (1 KB
   // each), then 128 token rows x 64 bf16 with the 16-byte chunk c of row r at
   // chunk c ^ ((r >> 1) & 7): the 64 banks span two 128-byte rows, so the 16
@@ -912,13 +925,18 @@ __global__ __launch_bounds__(kGemmThreads) void prefill_gemm_kernel(
 
     const int8_t* wstage0 = wbase + (size_t)ks0 * 1024;
     const int8_t* xstage0 = (const int8_t*)(act + (size_t)ks0 * 64);
-    // load i of stage s: packed tiles for i < 8, token row groups after
+    const int8_t* xstage0_lo = act_lo ? (const int8_t*)(act_lo + (size_t)ks0 * 64) : xstage0;
+    // load i of stage s: packed tiles for i < 8, token row groups after;
+    // stages nst .. 2*nst-1 (two-pass calls) repeat the weights over act_lo
     auto dma = [&](int s, int i) {
       const uint32_t so = (uint32_t)(s % kNStage) * kStageBytes;
-      if (i < kWaveTiles) return Dma{woff[i], wstage0 + (size_t)s * 1024, m0_w + so + i * 1024};
+      const bool lo = s >= nst;
+      const int sk = lo ? s - nst : s;
+      if (i < kWaveTiles) return Dma{woff[i], wstage0 + (size_t)sk * 1024, m0_w + so + i * 1024};
       const int r = i - kWaveTiles;
-      return Dma{xoff[r], xstage0 + (size_t)s * 128, m0_x + so + r * 1024};
+      return Dma{xoff[r], (lo ? xstage0_lo : xstage0) + (size_t)sk * 128, m0_x + so + r * 1024};
     };
+    const int nst_all = act_lo ? 2 * nst : nst;
 
     // every wave is done with the ring before it is refilled.  The previous
     // tile's stores may still be in flight: the counter waits below count
@@ -931,16 +949,16 @@ __global__ __launch_bounds__(kGemmThreads) void prefill_gemm_kernel(
     // loop when it holds at most 64 or 32 tokens
     if (nv > 64) {
       v4f acc[kWaveTiles][8];
-      tile_kloop<DUAL, 8>(acc, nst, dma, slot);
-      tile_epilogue<DUAL, 8>(acc, wave, lane, n0, N, R, C, p0, nv, blob, hout, ybase);
+      tile_kloop<DUAL, 8>(acc, nst_all, dma, slot);
+      tile_epilogue<DUAL, 8>(acc, wave, lane, n0, N, R, C, p0, nv, blob, hout, hout_lo, ybase);
     } else if (nv > 32) {
       v4f acc[kWaveTiles][4];
-      tile_kloop<DUAL, 4>(acc, nst, dma, slot);
-      tile_epilogue<DUAL, 4>(acc, wave, lane, n0, N, R, C, p0, nv, blob, hout, ybase);
+      tile_kloop<DUAL, 4>(acc, nst_all, dma, slot);
+      tile_epilogue<DUAL, 4>(acc, wave, lane, n0, N, R, C, p0, nv, blob, hout, hout_lo, ybase);
     } else {
       v4f acc[kWaveTiles][2];
-      tile_kloop<DUAL, 2>(acc, nst, dma, slot);
-      tile_epilogue<DUAL, 2>(acc, wave, lane, n0, N, R, C, p0, nv, blob, hout, ybase);
+      tile_kloop<DUAL, 2>(acc, nst_all, dma, slot);
+      tile_epilogue<DUAL, 2>(acc, wave, lane, n0, N, R, C, p0, nv, blob, hout, hout_lo, ybase);
     }
   }
 }
@@ -970,10 +988,15 @@ __global__ __launch_bounds__(256) void combine_kernel(int T, int C, int k, int S
   *(v4f*)(out + (size_t)t * C + c) = s;
 }
 
-__global__ __launch_bounds__(256) void f32_to_bf16_kernel(const float* __restrict__ x,
-                                                          uint16_t* __restrict__ y, size_t n) {
-  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256)
-    y[i] = f32_to_bf16_rne(x[i]);
+// fp32 activations as two bf16 parts: hi = bf16(x), lo = bf16(x - hi)
+__global__ __launch_bounds__(256) void f32_to_bf16_pair_kernel(const float* __restrict__ x,
+                                                               uint16_t* __restrict__ hi,
+                                                               uint16_t* __restrict__ lo, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) {
+    const uint32_t h = f32_to_bf16_rne(x[i]);
+    hi[i] = (uint16_t)h;
+    lo[i] = (uint16_t)f32_to_bf16_rne(x[i] - __uint_as_float(h << 16));
+  }
 }
 
 // Workgroups of kernel k that fit on one CU, queried once per process (the
@@ -999,13 +1022,19 @@ hipError_t launch_prefill(const mira_shape& s, const Layout& L, const WsPtr& w, 
                           const ExpertPool& ep, float* out, hipStream_t st) {
   const int T = L.T;
   if (T == 0) return hipSuccess;
+  // fp32 activations run both GEMMs in two passes (high and low bf16 parts
+  // of x, then of H'), bf16 activations in one
   const uint16_t* xb = (const uint16_t*)x;
+  const uint16_t* xlo = nullptr;
+  uint16_t* hlo = nullptr;
   if (s.act_dtype == MIRA_F32) {
     const size_t n = (size_t)T * L.C;
     const int blocks = (int)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096);
-    launch_timed("prefill_cvt", f32_to_bf16_kernel, dim3(blocks), dim3(256), 0, st, (const float*)x,
-                 w.xb16, n);
+    launch_timed("prefill_cvt", f32_to_bf16_pair_kernel, dim3(blocks), dim3(256), 0, st,
+                 (const float*)x, w.xb16, w.xlo16, n);
     xb = w.xb16;
+    xlo = w.xlo16;
+    hlo = w.hlo;
   }
   const size_t ysplit = (size_t)L.P * L.C;
   {
@@ -1015,7 +1044,7 @@ hipError_t launch_prefill(const mira_shape& s, const Layout& L, const WsPtr& w, 
     const long tiles = (long)L.mt_max * ((L.R + kTileRows / 2 - 1) / (kTileRows / 2));
     const int grid = persistent_grid(gemm_occupancy(kern, once, occ), tiles);
     launch_timed("prefill_gateup", kern, dim3(grid), dim3(kGemmThreads), 0, st, L.C, L.R, L.G, 1,
-                 ep, w.misc, w.offsets, w.tokpos, xb, w.hbuf, (float*)nullptr, (size_t)0);
+                 ep, w.misc, w.offsets, w.tokpos, xb, xlo, w.hbuf, hlo, (float*)nullptr, (size_t)0);
   }
   {
     auto kern = prefill_gemm_kernel<false>;
@@ -1025,7 +1054,7 @@ hipError_t launch_prefill(const mira_shape& s, const Layout& L, const WsPtr& w, 
     const int grid = persistent_grid(gemm_occupancy(kern, once, occ), tiles);
     launch_timed("prefill_down", kern, dim3(grid), dim3(kGemmThreads), 0, st, L.C, L.R, L.G,
                  L.ksplit, ep, w.misc, w.offsets, w.tokpos, (const uint16_t*)w.hbuf,
-                 (uint16_t*)nullptr, w.ybuf, ysplit);
+                 (const uint16_t*)hlo, (uint16_t*)nullptr, (uint16_t*)nullptr, w.ybuf, ysplit);
   }
   {
     dim3 grid((L.C / 4 + 255) / 256, T);
