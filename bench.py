@@ -54,13 +54,13 @@ PROF_EVERY = 8  # steps timed with events: one layer-copy rotation in every 8
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 TRAFFIC = {
     ("decode_gateup", "mixtral_decode"): dict(sources=("decode.hip", "decode_dev.h", "int4_format.h"),
-                                               sha="2509315552acff60", fetch_kib=114816.7, write_kib=98.0),
+                                               sha="78cc0bdc1329eef2", fetch_kib=114834.4, write_kib=110.3),
     ("decode_gateup", "mixtral_decode_int4"): dict(sources=("decode.hip", "decode_dev.h", "int4_format.h"),
-                                                    sha="2509315552acff60", fetch_kib=61055.8, write_kib=98.0),
-    ("prefill_gateup", "mixtral_prefill"): dict(sources=("prefill.hip",), sha="ccf7798229ccbdd1",
-                                                 fetch_kib=600861.8, write_kib=38338.1),
-    ("prefill_gateup", "fine_grained"): dict(sources=("prefill.hip",), sha="ccf7798229ccbdd1",
-                                              fetch_kib=290420.9, write_kib=57803.8),
+                                                    sha="78cc0bdc1329eef2", fetch_kib=61050.4, write_kib=98.1),
+    ("prefill_gateup", "mixtral_prefill"): dict(sources=("prefill.hip",), sha="8d87e7443ab4d714",
+                                                 fetch_kib=600413.4, write_kib=38203.4),
+    ("prefill_gateup", "fine_grained"): dict(sources=("prefill.hip",), sha="8d87e7443ab4d714",
+                                              fetch_kib=290638.8, write_kib=57853.3),
 }
 
 

@@ -29,7 +29,7 @@ constexpr int kXlUnroll = 16;  // k-steps per weight batch
 
 template <int NG, bool I4, bool XL>
 __device__ __forceinline__ void decode_gateup_body(int C, int R, const ExpertPool& ep,
-                                                   const DecodeWork* __restrict__ work,
+                                                   DecodeWork* __restrict__ work,
                                                    const int8_t* __restrict__ xdig,
                                                    int8_t* __restrict__ hdig,
                                                    int32_t* __restrict__ hexp) {
@@ -40,7 +40,10 @@ __device__ __forceinline__ void decode_gateup_body(int C, int R, const ExpertPoo
   const int g = wk.group;
   if (g < 0) return;
   const int slot = ep.slot_table[g];  // read now: the table may change after routing
-  if (slot < 0 || slot >= ep.n_slots) {
+  const bool ok = slot >= 0 && slot < ep.n_slots;
+  // block 0 of the expert keeps the resolved slot for the down kernel
+  if (rb == 0 && threadIdx.x == 0) work[a].slot = ok ? slot : -1;
+  if (!ok) {
     if (threadIdx.x == 0 && ep.status) atomicOr(ep.status, slot < 0 ? 1 : 2);
     return;
   }
@@ -64,7 +67,10 @@ __device__ __forceinline__ void decode_gateup_body(int C, int R, const ExpertPoo
     __shared__ __attribute__((aligned(16))) int8_t xl[16 * (kXlMaxC + 16)];
     const int ld = C + 16;
     const int chunks = C / 16;
-    for (int i = threadIdx.x; i < NG * 16 * chunks; i += 256) {
+    // only the digit rows of the group's tokens are staged; lanes of the
+    // other columns take a zero operand without reading LDS
+    const int rows = 3 * min(n, kTokPerGroup);
+    for (int i = threadIdx.x; i < rows * chunks; i += 256) {
       const int row = i / chunks, c16 = i - row * chunks;
       const int cg = row >> 4, col = row & 15;
       const int mm = col / 3, dd = col - 3 * mm, ti = cg * kTokPerGroup + mm;
@@ -77,7 +83,7 @@ __device__ __forceinline__ void decode_gateup_body(int C, int R, const ExpertPoo
     const int8_t* xr[NG];
 #pragma unroll
     for (int cg = 0; cg < NG; ++cg) xr[cg] = xl + (size_t)(cg * 16 + r16) * ld + kg * 16;
-    const auto load_x = [&](int cg, int ks) { return *(const v4i*)(xr[cg] + ks * 64); };
+    const auto load_x = [&](int cg, int ks) { return bv[cg] ? *(const v4i*)(xr[cg] + ks * 64) : zero16(); };
     gateup_block_i4<NG, kXlUnroll, true>(C, R, rb, (const uint8_t*)ep.pool + (size_t)slot * ep.stride,
                                          wk.off, bv, xev, load_x, hdig, hexp, bmax);
     return;
@@ -94,7 +100,7 @@ __device__ __forceinline__ void decode_gateup_body(int C, int R, const ExpertPoo
 
 template <int NG, bool I4>
 __global__ __launch_bounds__(256) void decode_gateup_kernel(int C, int R, ExpertPool ep,
-                                                            const DecodeWork* __restrict__ work,
+                                                            DecodeWork* __restrict__ work,
                                                             const int8_t* __restrict__ xdig,
                                                             int8_t* __restrict__ hdig,
                                                             int32_t* __restrict__ hexp) {
@@ -103,11 +109,54 @@ __global__ __launch_bounds__(256) void decode_gateup_kernel(int C, int R, Expert
 
 // The LDS variant keeps two workgroups per CU (the 64 KB of digits each).
 __global__ __launch_bounds__(256, 2) void decode_gateup_xl_kernel(int C, int R, ExpertPool ep,
-                                                                 const DecodeWork* __restrict__ work,
+                                                                 DecodeWork* __restrict__ work,
                                                                  const int8_t* __restrict__ xdig,
                                                                  int8_t* __restrict__ hdig,
                                                                  int32_t* __restrict__ hexp) {
   decode_gateup_body<1, true, true>(C, R, ep, work, xdig, hdig, hexp);
+}
+
+// One-token calls: every wave streams one 16-row tile of the concatenated
+// rows of the active experts (tile t = expert a, rows 16*(t mod R/16) ..)
+// and writes that tile's H' with its own exponent (h_tile_1tok), so no wave
+// waits for another and the host splits the tiles evenly over the CUs (W
+// waves per workgroup, about one workgroup per CU).  The wave of tile 0 of
+// each expert also stores the slot it resolved from the table in the
+// expert's descriptor (-1 if invalid), for the down kernel.
+constexpr int kTileMaxWaves = 8;
+
+__global__ __launch_bounds__(64 * kTileMaxWaves) void decode_gateup_tile_kernel(
+    int C, int R, int W, int ntiles, ExpertPool ep, DecodeWork* __restrict__ work,
+    const int8_t* __restrict__ xdig, int8_t* __restrict__ hdig, int32_t* __restrict__ hexp) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int t = blockIdx.x * W + wave;
+  if (wave >= W || t >= ntiles) return;
+  const int tpe = R / 16;
+  const int a = t / tpe, rt = t - a * tpe;
+  const DecodeWork& wk = work[a];
+  const int g = wk.group;
+  if (g < 0) return;
+  const int slot = ep.slot_table[g];  // read now: the table may change after routing
+  const bool ok = slot >= 0 && slot < ep.n_slots;
+  if (rt == 0 && lane == 0) work[a].slot = ok ? slot : -1;
+  if (!ok) {
+    if (lane == 0 && ep.status) atomicOr(ep.status, slot < 0 ? 1 : 2);
+    return;
+  }
+  const int r16 = lane & 15, kg = lane >> 4;
+  const bool bv = r16 < 3 && wk.n > 0;
+  const int tok = bv ? wk.tok[0] : 0;
+  const int xe = bv ? wk.xe[0] : 0;
+  const int8_t* bp = xdig + ((size_t)tok * kDigits + (bv ? r16 : 0)) * C + kg * 16;
+  const auto load_b = [&](int, int ks) { return ld16(bp + ks * 64); };
+  // seven 16-row tiles per CU at Mixtral's shape: one wave per tile beat two
+  // waves per tile (gate and up streamed apart, up sums handed over in LDS)
+  // by 0.45 us per call
+  v4i accg[1], accu[1];
+  float sg[4];
+  const bool bva[1] = {bv};
+  gateup_tile_stream<1>(C, R, rt, ep.pool + (size_t)slot * ep.stride, bva, load_b, accg, accu, sg);
+  h_tile_1tok(R, rt, wk.off, bv, xe, accg[0], accu[0], sg, hdig, hexp);
 }
 
 // ---------------------------------------------------------------------------
@@ -120,7 +169,7 @@ __global__ __launch_bounds__(256, 2) void decode_gateup_xl_kernel(int C, int R, 
 // tokens of three digits or 8 of two (column r16 = token r16/HD of the
 // group, digit r16%HD), and NG groups cover that many tokens per group.
 // ---------------------------------------------------------------------------
-template <int NG, int KS, bool I4, int HD>
+template <int NG, int KS, bool I4, int HD, bool TE>
 __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
     int C, int R, int T, int max_active, ExpertPool ep, const DecodeWork* __restrict__ work,
     const int8_t* __restrict__ hdig, const int32_t* __restrict__ hexp, float* __restrict__ out) {
@@ -130,7 +179,11 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
   for (int i = tid; i < KS * MIRA_DECODE_MAX_TOKENS * 16; i += 64 * KS) (&part[0][0][0])[i] = 0.f;
   __syncthreads();
 
+  static_assert(!TE || (NG == 1 && HD == 3), "per-tile exponents: one token, three digits");
   const int r16 = lane & 15, kg = lane >> 4;
+  // TE: column r16 < 12 is digit d of the k-step's tile j = r16/3 (k group
+  // j), so each tile's digits carry their own exponent; otherwise column
+  // r16 is digit d of token m
   const int m = r16 / HD, d = r16 - HD * m;
   const int nks = R / 64;
   // k-steps per wave; even for INT4, whose loads cover two k-steps
@@ -139,9 +192,9 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
 
   for (int a = 0; a < max_active; ++a) {
     const DecodeWork& wk = work[a];
-    const int g = wk.group;
-    if (g < 0) break;
-    const int slot = ep.slot_table[g];
+    if (wk.group < 0) break;
+    // the slot the gate/up kernel resolved from the table (-1 if invalid)
+    const int slot = wk.slot;
     if (slot < 0 || slot >= ep.n_slots) continue;
     const int off = wk.off, n = wk.n;
     // tile row c0/16 of the down matrix: INT8 tiles of 1 KB (lane l at 16*l),
@@ -158,11 +211,24 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
     bool bv[NG];
 #pragma unroll
     for (int cg = 0; cg < NG; ++cg) {
-      const int i = cg * TPG + m;
-      bv[cg] = r16 < HD * TPG && i < n;
+      const int i = TE ? 0 : cg * TPG + m;
+      bv[cg] = (TE ? r16 < 12 : r16 < HD * TPG) && i < n;
       const size_t pos = (size_t)off + (bv[cg] ? i : 0);
       bp[cg] = hdig + (pos * HD + d) * R + kg * 16;
-      hx[cg] = hexp + pos * nks;
+      hx[cg] = TE ? hexp + pos * (R / 16) + m : hexp + pos * nks;
+    }
+    // TE: only the lanes of k group j load their tile's digits
+    const bool bload = !TE || kg == m;
+    // the combine's token and weight, loaded ahead of the stream so that
+    // they return with the first batch
+    int ctok[NG];
+    float cwgt[NG];
+#pragma unroll
+    for (int cg = 0; cg < NG; ++cg) {
+      const bool lead = (TE ? r16 == 0 : d == 0) && bv[cg];
+      const int ti = TE ? 0 : cg * TPG + m;
+      ctok[cg] = lead ? wk.tok[ti] : 0;
+      cwgt[cg] = lead ? wk.w[ti] : 0.f;
     }
     float facc[NG][4];
 #pragma unroll
@@ -196,8 +262,8 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
         if constexpr (!I4) bt.a[u] = in ? ld16_stream(dp + ks * 1024) : zero16();
 #pragma unroll
         for (int cg = 0; cg < NG; ++cg) {
-          bt.b[u][cg] = (in && bv[cg]) ? ld16(bp[cg] + ks * 64) : zero16();
-          bt.he[u][cg] = (in && bv[cg]) ? hx[cg][ks] : 0;
+          bt.b[u][cg] = (in && bv[cg] && bload) ? ld16(bp[cg] + ks * 64) : zero16();
+          bt.he[u][cg] = (in && bv[cg]) ? hx[cg][TE ? 4 * ks : ks] : 0;
         }
       }
     };
@@ -233,15 +299,22 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
     }
 #pragma unroll
     for (int cg = 0; cg < NG; ++cg) {
-      const int ti = cg * TPG + m;
-      const bool lead = d == 0 && bv[cg];
-      const int t = lead ? wk.tok[ti] : 0;
-      const float wgt = lead ? wk.w[ti] : 0.f;
+      const bool lead = (TE ? r16 == 0 : d == 0) && bv[cg];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        float v = facc[cg][i] + __shfl_down(facc[cg][i], 1, 64);
-        if constexpr (HD == 3) v += __shfl_down(facc[cg][i], 2, 64);
-        if (lead) part[wave][t][kg * 4 + i] += wgt * v;
+        float v;
+        if constexpr (TE) {
+          // the twelve (tile, digit) columns of the row (lanes 12-15 hold 0)
+          v = facc[cg][i];
+          v += __shfl_xor(v, 1, 64);
+          v += __shfl_xor(v, 2, 64);
+          v += __shfl_xor(v, 4, 64);
+          v += __shfl_xor(v, 8, 64);
+        } else {
+          v = facc[cg][i] + __shfl_down(facc[cg][i], 1, 64);
+          if constexpr (HD == 3) v += __shfl_down(facc[cg][i], 2, 64);
+        }
+        if (lead) part[wave][ctok[cg]][kg * 4 + i] += cwgt[cg] * v;
       }
     }
   }
@@ -259,10 +332,10 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
 // batches of half the size (INT4 down 20.5 -> 18.0 us, INT8 unchanged)
 constexpr int kDownKS = 16;
 
-template <int NG, bool I4, int HD>
+template <int NG, bool I4, int HD, bool TE = false>
 static void launch_decode_down_ng(const Layout& L, const WsPtr& w, const ExpertPool& ep,
                                   float* out, hipStream_t st) {
-  launch_timed("decode_down", (decode_down_kernel<NG, kDownKS, I4, HD>), dim3(L.C / 16),
+  launch_timed("decode_down", (decode_down_kernel<NG, kDownKS, I4, HD, TE>), dim3(L.C / 16),
                dim3(64 * kDownKS), 0, st, L.C, L.R, L.T, decode_max_active(L), ep, w.dwork, w.hdig,
                w.hexp, out);
 }
@@ -283,9 +356,27 @@ static void launch_decode_gateup(const Layout& L, const WsPtr& w, const ExpertPo
                dim3(256), 0, st, L.C, L.R, ep, w.dwork, w.xdig, w.hdig, w.hexp);
 }
 
+// One token: the 16-row tiles of all active experts split evenly over the
+// CUs (W waves per workgroup, about one workgroup per CU), and the down
+// kernel reads per-tile exponents.
+static void launch_decode_ffn_1tok(const Layout& L, const WsPtr& w, const ExpertPool& ep,
+                                   float* out, hipStream_t st) {
+  const int ntiles = decode_max_active(L) * (L.R / 16);
+  const int cus = device_cu_count();
+  const int W = std::min(kTileMaxWaves, (ntiles + cus - 1) / cus);
+  const int nwg = (ntiles + W - 1) / W;
+  launch_timed("decode_gateup", decode_gateup_tile_kernel, dim3(nwg), dim3(64 * W), 0, st, L.C,
+               L.R, W, ntiles, ep, w.dwork, w.xdig, w.hdig, w.hexp);
+  launch_decode_down_ng<1, false, 3, true>(L, w, ep, out, st);
+}
+
 template <bool I4>
 static void launch_decode_ffn(const Layout& L, const WsPtr& w, const ExpertPool& ep, float* out,
                               hipStream_t st) {
+  if (!I4 && L.T == 1) {
+    launch_decode_ffn_1tok(L, w, ep, out, st);
+    return;
+  }
   // token groups of an expert (each holds at most T tokens): 5 tokens per x
   // operand; H' in three digits for one x group (5 tokens per operand),
   // else in two (8 tokens per operand)

@@ -82,33 +82,32 @@ __device__ __forceinline__ void write_h_digits(int R, int rb, int off, bool lead
   }
 }
 
-// Gate/up + SwiGLU of one block of 64 expert rows (rb) for the tokens of one
-// expert group, by a workgroup of 4 waves (wave w owns rows rb*64 + 16w ..
-// +15).  Token column r16 of operand group cg is token cg*5 + r16/3, digit
-// r16%3; bv[cg] says whether that column holds a token and xev[cg] is the
-// token's fixed-point exponent.  load_b(cg, ks) returns this lane's 16 digit
-// bytes of k-step ks (k = 64*ks + 16*(lane/16) .. +15).  Writes H' of the
-// group's positions off .. off+n-1 as per-block fixed-point digits
-// (write_h_digits).
+// Gate and up sums of one 16-row tile (rows 16*rtile .. +15) for the tokens
+// of one expert group, by one wave.  Token column r16 of operand group cg is
+// token cg*5 + r16/3, digit r16%3; bv[cg] says whether that column holds a
+// token.  load_b(cg, ks) returns this lane's 16 digit bytes of k-step ks
+// (k = 64*ks + 16*(lane/16) .. +15).  On return accg/accu hold the int32
+// digit sums of rows 16*rtile + 4*(lane/16) + i (i < 4) for column r16, and
+// sg those rows' scales sigma_r.
 template <int NG, typename LoadB>
-__device__ __forceinline__ void gateup_block(int C, int R, int rb, const int8_t* __restrict__ blob,
-                                             int off, const bool (&bv)[NG], const int (&xev)[NG],
-                                             LoadB load_b, int8_t* __restrict__ hdig,
-                                             int32_t* __restrict__ hexp,
-                                             float (*bmax)[NG * kTokPerGroup]) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r16 = lane & 15, kg = lane >> 4;
-  const int m = r16 / 3, d = r16 - 3 * m;
-  // this wave's 16-row tile: 1 KB per k-step, lane l at byte 16*l
-  const int rtile = rb * (kBlk / 16) + wave;
+__device__ __forceinline__ void gateup_tile_stream(int C, int R, int rtile,
+                                                   const int8_t* __restrict__ blob,
+                                                   const bool (&bv)[NG], LoadB load_b,
+                                                   v4i (&accg)[NG], v4i (&accu)[NG],
+                                                   float (&sg)[4]) {
+  const int lane = threadIdx.x & 63, kg = lane >> 4;
+  // the tile: 1 KB per k-step, lane l at byte 16*l
   const int8_t* gp = blob + (size_t)rtile * (C / 64) * 1024 + lane * 16;
   const int8_t* up = gp + (size_t)R * C;
+  // the four bf16 scales of this lane's rows are one 8-byte load, issued
+  // ahead of the stream so that it returns with the first batch instead of
+  // costing a round trip at the end
+  const int rbase = rtile * 16 + kg * 4;
+  const uint2 sraw = *(const uint2*)(blob + (size_t)3 * R * C + (size_t)rbase * 2);
 
-  v4i accg[NG], accu[NG];
 #pragma unroll
   for (int cg = 0; cg < NG; ++cg) accg[cg] = accu[cg] = zero16();
 
-  // two batches of U k-steps in flight: issue one, consume the other
   constexpr int kDecUnroll = dec_unroll(NG);
   const int nks = C / 64;
   struct Batch {
@@ -143,12 +142,39 @@ __device__ __forceinline__ void gateup_block(int C, int R, int rb, const int8_t*
     consume(bt);
   }
 
-  // epilogue: rows rbase+i (i < 4) for token column r16
-  const int rbase = rb * kBlk + wave * 16 + kg * 4;
-  const uint16_t* sig = (const uint16_t*)(blob + (size_t)3 * R * C);
+  sg[0] = __uint_as_float(sraw.x << 16);
+  sg[1] = __uint_as_float(sraw.x & 0xffff0000u);
+  sg[2] = __uint_as_float(sraw.y << 16);
+  sg[3] = __uint_as_float(sraw.y & 0xffff0000u);
+}
+
+// H' of one row from its gate and up digit sums: with xs = 2^-E of the
+// token's fixed point, G = sigma*xs*gsum, U = sigma*xs*usum and
+// H' = sigma * silu(G) * U (the shared scale of down column r).
+__device__ __forceinline__ float swiglu_h(int gsum_digits, int usum_digits, float xs, float sig) {
+  const float gv = combine_digits_i(gsum_digits) * xs * sig;
+  const float uv = combine_digits_i(usum_digits) * xs * sig;
+  return sig * (gv / (1.f + expf(-gv)) * uv);
+}
+
+// Gate/up + SwiGLU of one block of 64 expert rows (rb) for the tokens of one
+// expert group, by a workgroup of 4 waves (wave w owns rows rb*64 + 16w ..
+// +15, streamed by gateup_tile_stream); xev[cg] is the token's fixed-point
+// exponent.  Writes H' of the group's positions off .. off+n-1 as per-block
+// fixed-point digits (write_h_digits).
+template <int NG, typename LoadB>
+__device__ __forceinline__ void gateup_block(int C, int R, int rb, const int8_t* __restrict__ blob,
+                                             int off, const bool (&bv)[NG], const int (&xev)[NG],
+                                             LoadB load_b, int8_t* __restrict__ hdig,
+                                             int32_t* __restrict__ hexp,
+                                             float (*bmax)[NG * kTokPerGroup]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kg = lane >> 4;
+  const int m = r16 / 3, d = r16 - 3 * m;
+  v4i accg[NG], accu[NG];
   float sg[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) sg[i] = bf16_to_f32(sig[rbase + i]);
+  gateup_tile_stream<NG>(C, R, rb * (kBlk / 16) + wave, blob, bv, load_b, accg, accu, sg);
+
   const bool lead = d == 0;
   float hv[NG][4];
 #pragma unroll
@@ -157,12 +183,8 @@ __device__ __forceinline__ void gateup_block(int C, int R, int rb, const int8_t*
     float mx = 0.f;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float gsum = combine_digits_i(accg[cg][i]);
-      const float usum = combine_digits_i(accu[cg][i]);
-      const float gv = gsum * xs * sg[i];
-      const float uv = usum * xs * sg[i];
-      const float h = gv / (1.f + expf(-gv)) * uv;
-      hv[cg][i] = (lead && bv[cg]) ? sg[i] * h : 0.f;
+      const float h = swiglu_h(accg[cg][i], accu[cg][i], xs, sg[i]);
+      hv[cg][i] = (lead && bv[cg]) ? h : 0.f;
       mx = fmaxf(mx, fabsf(hv[cg][i]));
     }
     mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
@@ -170,6 +192,52 @@ __device__ __forceinline__ void gateup_block(int C, int R, int rb, const int8_t*
     if (kg == 0 && lead && r16 < 3 * kTokPerGroup) bmax[wave][cg * kTokPerGroup + m] = mx;
   }
   write_h_digits<NG>(R, rb, off, lead, bv, hv, hdig, hexp, bmax);
+}
+
+// One-token groups: H' of one 16-row tile (rows 16*rt .. +15) from its gate
+// and up digit sums (lane (r16, kg) holds rows 16*rt + 4*kg + i of digit
+// column r16), with the tile's own exponent: three balanced base-256 digits
+// hdig[(pos*3 + d)*R + r] with kFixBits bits against the tile maximum and
+// hexp[pos*(R/16) + rt].  (The down kernel gives each (tile, digit) pair of a
+// k-step its own operand column, so the four tiles of a k-step need no
+// common exponent.)  sg: the rows' scales sigma_r; xe: the token's
+// fixed-point exponent.
+__device__ __forceinline__ void h_tile_1tok(int R, int rt, int pos, bool bv, int xe, v4i accg,
+                                            v4i accu, const float (&sg)[4],
+                                            int8_t* __restrict__ hdig,
+                                            int32_t* __restrict__ hexp) {
+  const int lane = threadIdx.x & 63;
+  const int r16 = lane & 15, kg = lane >> 4;
+  // lane r16 == 0 of each row group holds the token's rows 4*kg .. +3
+  const bool lead = bv && r16 == 0;
+  const float xs = bv ? ldexpf(1.f, -xe) : 0.f;
+  float hv[4], mx = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float h = swiglu_h(accg[i], accu[i], xs, sg[i]);
+    hv[i] = lead ? h : 0.f;
+    mx = fmaxf(mx, fabsf(hv[i]));
+  }
+  mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  if (!lead) return;
+  const int Eh = kFixBits - exp_bound(mx);
+  uint32_t w0 = 0, w1 = 0, w2 = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    // |hv| <= mx < 2^exp_bound(mx): |v| <= 2^22, so the top digit stays
+    // within [-64, 64]
+    int d0, d1, d2;
+    split_digits((int)rintf(ldexpf(hv[i], Eh)), d0, d1, d2);
+    w0 |= (uint32_t)(d0 & 0xFF) << (8 * i);
+    w1 |= (uint32_t)(d1 & 0xFF) << (8 * i);
+    w2 |= (uint32_t)(d2 & 0xFF) << (8 * i);
+  }
+  int8_t* hp = hdig + (size_t)pos * 3 * R + rt * 16 + kg * 4;
+  *(uint32_t*)(hp) = w0;
+  *(uint32_t*)(hp + R) = w1;
+  *(uint32_t*)(hp + 2 * (size_t)R) = w2;
+  if (kg == 0) hexp[(size_t)pos * (R / 16) + rt] = Eh;
 }
 
 // ---- INT4 variant (MIRA_FLAG_INT4) -----------------------------------------

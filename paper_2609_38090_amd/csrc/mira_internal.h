@@ -58,7 +58,8 @@ struct Layout {
 // preparation kernel so that each expert kernel starts from a single load.
 struct DecodeWork {
   int32_t group;  // expert (routed 0..E-1, shared E..E+S-1); -1 = no work
-  int32_t slot;   // slot seen by the routing (the expert kernels re-read the table)
+  int32_t slot;   // slot seen by the routing; the gate/up kernel replaces it with the slot it
+                  // resolved from the table (-1 if invalid), which the down kernel uses
   int32_t off;    // first permuted position of the group
   int32_t n;      // positions (tokens) of the group, <= MIRA_DECODE_MAX_TOKENS
   int32_t tok[MIRA_DECODE_MAX_TOKENS];  // token of position off+i
@@ -127,7 +128,8 @@ inline Layout make_layout(const mira_shape& s, int T) {
   L.dwork = take(G * sizeof(DecodeWork));
   L.xdig = take((size_t)L.Td * kDigits * L.C);
   L.hdig = take((size_t)L.Pd * kDigits * L.R);  // room for three digits
-  L.hexp = take((size_t)L.Pd * (L.R / kBlk) * 4);
+  // H' exponents: one per 64-row block, or per 16-row tile for one token
+  L.hexp = take((size_t)L.Pd * (L.Td == 1 ? L.R / 16 : L.R / kBlk) * 4);
   // fp32 activations: x and H' as high and low bf16 parts (two-pass GEMMs)
   const bool f32 = s.act_dtype == MIRA_F32;
   L.xb16 = take(f32 ? Tz * L.C * 2 : 0);
