@@ -159,6 +159,58 @@ __global__ __launch_bounds__(64 * kTileMaxWaves) void decode_gateup_tile_kernel(
   h_tile_1tok(R, rt, wk.off, bv, xe, accg[0], accu[0], sg, hdig, hexp);
 }
 
+// One-token INT4 calls (C <= kXlMaxC): the same tile split, with the
+// token's three digit rows copied into LDS once per workgroup (row stride
+// C + 16 bytes), so a wave's batches hold only weight registers.  A one-token
+// call's only token is token 0, whatever expert a tile belongs to.
+__global__ __launch_bounds__(64 * kTileMaxWaves) void decode_gateup_tile_i4_kernel(
+    int C, int R, int W, int ntiles, ExpertPool ep, DecodeWork* __restrict__ work,
+    const int8_t* __restrict__ xdig, int8_t* __restrict__ hdig, int32_t* __restrict__ hexp) {
+  __shared__ __attribute__((aligned(16))) int8_t xl[kDigits * (kXlMaxC + 16)];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int ld = C + 16, chunks = C / 16;
+  for (int i = threadIdx.x; i < kDigits * chunks; i += blockDim.x) {
+    const int row = i / chunks, c16 = i - row * chunks;
+    *(v4i*)(xl + (size_t)row * ld + c16 * 16) = ld16(xdig + (size_t)row * C + c16 * 16);
+  }
+  __syncthreads();
+  const int t = blockIdx.x * W + wave;
+  if (wave >= W || t >= ntiles) return;
+  const int tpe = R / 16;
+  const int a = t / tpe, rt = t - a * tpe;
+  const DecodeWork& wk = work[a];
+  const int g = wk.group;
+  if (g < 0) return;
+  const int slot = ep.slot_table[g];  // read now: the table may change after routing
+  const bool ok = slot >= 0 && slot < ep.n_slots;
+  if (rt == 0 && lane == 0) work[a].slot = ok ? slot : -1;
+  if (!ok) {
+    if (lane == 0 && ep.status) atomicOr(ep.status, slot < 0 ? 1 : 2);
+    return;
+  }
+  const int r16 = lane & 15, kg = lane >> 4;
+  const bool bv = r16 < 3 && wk.n > 0;
+  const int xe = bv ? wk.xe[0] : 0;
+  const int8_t* xr = xl + (size_t)(bv ? r16 : 0) * ld + kg * 16;
+  const auto load_x = [&](int, int ks) { return bv ? *(const v4i*)(xr + ks * 64) : zero16(); };
+  float accg[1][4], accu[1][4];
+  const bool bva[1] = {bv};
+  gateup_tile_stream_i4<1, kXlUnroll, true>(C, R, rt, (const uint8_t*)ep.pool + (size_t)slot * ep.stride,
+                                            bva, load_x, accg, accu);
+  // 2^-E of the token's fixed point, and 1/16 for the nibble operand (16*q)
+  const bool lead = bv && r16 == 0;
+  const float xs = bv ? ldexpf(1.f, -xe - 4) : 0.f;
+  float hv[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float gv = combine_digits_f(accg[0][i]) * xs;
+    const float uv = combine_digits_f(accu[0][i]) * xs;
+    const float h = gv / (1.f + expf(-gv)) * uv;
+    hv[i] = lead ? h : 0.f;
+  }
+  write_h_tile_1tok(R, rt, wk.off, lead, hv, hdig, hexp);
+}
+
 // ---------------------------------------------------------------------------
 // Down projection + weighted combine.  Workgroup = 16 output rows c; its KS
 // waves split the R dimension.  For every non-empty expert, y = Qd H' with
@@ -176,8 +228,9 @@ __global__ __launch_bounds__(64 * KS) void decode_down_kernel(
   constexpr int TPG = h_tok_per_group(HD);
   __shared__ float part[KS][MIRA_DECODE_MAX_TOKENS][16];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int i = tid; i < KS * MIRA_DECODE_MAX_TOKENS * 16; i += 64 * KS) (&part[0][0][0])[i] = 0.f;
-  __syncthreads();
+  // each wave adds only into its own slice, so it clears only that slice and
+  // nothing waits before the stream starts
+  for (int i = lane; i < MIRA_DECODE_MAX_TOKENS * 16; i += 64) (&part[wave][0][0])[i] = 0.f;
 
   static_assert(!TE || (NG == 1 && HD == 3), "per-tile exponents: one token, three digits");
   const int r16 = lane & 15, kg = lane >> 4;
@@ -359,22 +412,24 @@ static void launch_decode_gateup(const Layout& L, const WsPtr& w, const ExpertPo
 // One token: the 16-row tiles of all active experts split evenly over the
 // CUs (W waves per workgroup, about one workgroup per CU), and the down
 // kernel reads per-tile exponents.
+template <bool I4>
 static void launch_decode_ffn_1tok(const Layout& L, const WsPtr& w, const ExpertPool& ep,
                                    float* out, hipStream_t st) {
   const int ntiles = decode_max_active(L) * (L.R / 16);
   const int cus = device_cu_count();
   const int W = std::min(kTileMaxWaves, (ntiles + cus - 1) / cus);
   const int nwg = (ntiles + W - 1) / W;
-  launch_timed("decode_gateup", decode_gateup_tile_kernel, dim3(nwg), dim3(64 * W), 0, st, L.C,
-               L.R, W, ntiles, ep, w.dwork, w.xdig, w.hdig, w.hexp);
-  launch_decode_down_ng<1, false, 3, true>(L, w, ep, out, st);
+  launch_timed("decode_gateup", I4 ? decode_gateup_tile_i4_kernel : decode_gateup_tile_kernel,
+               dim3(nwg), dim3(64 * W), 0, st, L.C, L.R, W, ntiles, ep, w.dwork, w.xdig, w.hdig,
+               w.hexp);
+  launch_decode_down_ng<1, I4, 3, true>(L, w, ep, out, st);
 }
 
 template <bool I4>
 static void launch_decode_ffn(const Layout& L, const WsPtr& w, const ExpertPool& ep, float* out,
                               hipStream_t st) {
-  if (!I4 && L.T == 1) {
-    launch_decode_ffn_1tok(L, w, ep, out, st);
+  if (L.T == 1 && (!I4 || L.C <= kXlMaxC)) {
+    launch_decode_ffn_1tok<I4>(L, w, ep, out, st);
     return;
   }
   // token groups of an expert (each holds at most T tokens): 5 tokens per x

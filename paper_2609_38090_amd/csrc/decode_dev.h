@@ -194,30 +194,20 @@ __device__ __forceinline__ void gateup_block(int C, int R, int rb, const int8_t*
   write_h_digits<NG>(R, rb, off, lead, bv, hv, hdig, hexp, bmax);
 }
 
-// One-token groups: H' of one 16-row tile (rows 16*rt .. +15) from its gate
-// and up digit sums (lane (r16, kg) holds rows 16*rt + 4*kg + i of digit
-// column r16), with the tile's own exponent: three balanced base-256 digits
+// One-token groups: writes H' of one 16-row tile (rows 16*rt .. +15) with
+// the tile's own exponent: three balanced base-256 digits
 // hdig[(pos*3 + d)*R + r] with kFixBits bits against the tile maximum and
-// hexp[pos*(R/16) + rt].  (The down kernel gives each (tile, digit) pair of a
-// k-step its own operand column, so the four tiles of a k-step need no
-// common exponent.)  sg: the rows' scales sigma_r; xe: the token's
-// fixed-point exponent.
-__device__ __forceinline__ void h_tile_1tok(int R, int rt, int pos, bool bv, int xe, v4i accg,
-                                            v4i accu, const float (&sg)[4],
-                                            int8_t* __restrict__ hdig,
-                                            int32_t* __restrict__ hexp) {
-  const int lane = threadIdx.x & 63;
-  const int r16 = lane & 15, kg = lane >> 4;
-  // lane r16 == 0 of each row group holds the token's rows 4*kg .. +3
-  const bool lead = bv && r16 == 0;
-  const float xs = bv ? ldexpf(1.f, -xe) : 0.f;
-  float hv[4], mx = 0.f;
+// hexp[pos*(R/16) + rt].  Lane (r16, kg) with lead set holds the token's
+// rows 16*rt + 4*kg + i in hv (hv = 0 elsewhere); the lead lanes are r16 ==
+// 0.  (The down kernel gives each (tile, digit) pair of a k-step its own
+// operand column, so the four tiles of a k-step need no common exponent.)
+__device__ __forceinline__ void write_h_tile_1tok(int R, int rt, int pos, bool lead,
+                                                  const float (&hv)[4], int8_t* __restrict__ hdig,
+                                                  int32_t* __restrict__ hexp) {
+  const int lane = threadIdx.x & 63, kg = lane >> 4;
+  float mx = 0.f;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const float h = swiglu_h(accg[i], accu[i], xs, sg[i]);
-    hv[i] = lead ? h : 0.f;
-    mx = fmaxf(mx, fabsf(hv[i]));
-  }
+  for (int i = 0; i < 4; ++i) mx = fmaxf(mx, fabsf(hv[i]));
   mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
   mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
   if (!lead) return;
@@ -238,6 +228,26 @@ __device__ __forceinline__ void h_tile_1tok(int R, int rt, int pos, bool bv, int
   *(uint32_t*)(hp + R) = w1;
   *(uint32_t*)(hp + 2 * (size_t)R) = w2;
   if (kg == 0) hexp[(size_t)pos * (R / 16) + rt] = Eh;
+}
+
+// One-token INT8 tile: H' = sigma (.) silu(G) (.) U from the gate and up
+// digit sums (lane (r16, kg) holds rows 16*rt + 4*kg + i of digit column
+// r16), written by write_h_tile_1tok.  sg: the rows' scales sigma_r; xe: the
+// token's fixed-point exponent.
+__device__ __forceinline__ void h_tile_1tok(int R, int rt, int pos, bool bv, int xe, v4i accg,
+                                            v4i accu, const float (&sg)[4],
+                                            int8_t* __restrict__ hdig,
+                                            int32_t* __restrict__ hexp) {
+  const int r16 = threadIdx.x & 15;
+  const bool lead = bv && r16 == 0;
+  const float xs = bv ? ldexpf(1.f, -xe) : 0.f;
+  float hv[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float h = swiglu_h(accg[i], accu[i], xs, sg[i]);
+    hv[i] = lead ? h : 0.f;
+  }
+  write_h_tile_1tok(R, rt, pos, lead, hv, hdig, hexp);
 }
 
 // ---- INT4 variant (MIRA_FLAG_INT4) -----------------------------------------
@@ -271,33 +281,28 @@ __device__ __forceinline__ float combine_digits_f(float s0) {
   return s2 * 65536.f + s1 * 256.f + s0;
 }
 
-// Gate/up + SwiGLU of one block of 64 expert rows for INT4 experts: the same
-// work split, operands and output as gateup_block.  Each k-step is one
+// Gate and up sums of one 16-row INT4 tile (rows 16*rtile .. +15) by one
+// wave, with the operands of gateup_tile_stream.  Each k-step is one
 // 64-column group: the MFMA sums of that group are scaled by the group's
-// fp16 scale (per row) and accumulated in fp32; H' = silu(G) (.) U (no shared
-// scale to fold).  U k-steps per load batch; with B_AT_USE the activation
-// digits are read (from LDS) right before their MFMAs instead of travelling
-// with the weight loads, so a batch holds only weight registers.
+// fp16 scale (per row) and accumulated in fp32 (accg/accu, still per digit
+// column).  U k-steps per load batch; with B_AT_USE the activation digits
+// are read (from LDS) right before their MFMAs instead of travelling with
+// the weight loads, so a batch holds only weight registers.
 template <int NG, int U, bool B_AT_USE, typename LoadB>
-__device__ __forceinline__ void gateup_block_i4(int C, int R, int rb, const uint8_t* __restrict__ blob,
-                                                int off, const bool (&bv)[NG], const int (&xev)[NG],
-                                                LoadB load_b, int8_t* __restrict__ hdig,
-                                                int32_t* __restrict__ hexp,
-                                                float (*bmax)[NG * kTokPerGroup]) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r16 = lane & 15, kg = lane >> 4;
-  const int m = r16 / 3, d = r16 - 3 * m;
+__device__ __forceinline__ void gateup_tile_stream_i4(int C, int R, int rtile,
+                                                      const uint8_t* __restrict__ blob,
+                                                      const bool (&bv)[NG], LoadB load_b,
+                                                      float (&accg)[NG][4], float (&accu)[NG][4]) {
+  const int lane = threadIdx.x & 63, kg = lane >> 4;
   const int nks = C / 64, npair = C / 128;
-  const int rtile = rb * (kBlk / 16) + wave;
-  // this wave's tile-row: nibble tiles of two groups (lane l's 16 bytes at
-  // 16*l) and the 32-byte scale blocks of its groups
+  // the tile-row: nibble tiles of two groups (lane l's 16 bytes at 16*l)
+  // and the 32-byte scale blocks of its groups
   const size_t mbytes = i4_matrix_bytes(R, C), nbytes = i4_nib_bytes(R, C);
   const uint8_t* gq = blob + (size_t)rtile * npair * kI4PairTile + lane * 16;
   const uint8_t* uq = gq + mbytes;
   const uint8_t* gs = blob + nbytes + (size_t)rtile * nks * 32 + lane * 8;
   const uint8_t* us = gs + mbytes;
 
-  float accg[NG][4], accu[NG][4];
 #pragma unroll
   for (int cg = 0; cg < NG; ++cg)
 #pragma unroll
@@ -371,6 +376,23 @@ __device__ __forceinline__ void gateup_block_i4(int C, int R, int rb, const uint
     issue(bt, ks);
     consume(bt);
   }
+}
+
+// Gate/up + SwiGLU of one block of 64 expert rows for INT4 experts: the same
+// work split, operands and output as gateup_block; each wave streams its
+// tile with gateup_tile_stream_i4, and H' = silu(G) (.) U (no shared scale to
+// fold).
+template <int NG, int U, bool B_AT_USE, typename LoadB>
+__device__ __forceinline__ void gateup_block_i4(int C, int R, int rb, const uint8_t* __restrict__ blob,
+                                                int off, const bool (&bv)[NG], const int (&xev)[NG],
+                                                LoadB load_b, int8_t* __restrict__ hdig,
+                                                int32_t* __restrict__ hexp,
+                                                float (*bmax)[NG * kTokPerGroup]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kg = lane >> 4;
+  const int m = r16 / 3, d = r16 - 3 * m;
+  float accg[NG][4], accu[NG][4];
+  gateup_tile_stream_i4<NG, U, B_AT_USE>(C, R, rb * (kBlk / 16) + wave, blob, bv, load_b, accg, accu);
 
   const bool lead = d == 0;
   float hv[NG][4];
