@@ -400,6 +400,28 @@ __global__ __launch_bounds__(kBigThreads) void permute_kernel(const int32_t* __r
 // base-256 digits; layout xdig[(t*3 + d)*C + c]; the exponent E_t goes into
 // the expert descriptors).
 // ---------------------------------------------------------------------------
+// Fixed-point digits (exponent Ex) of elements 4*i .. 4*i+3 of one token's x
+// row xr, into that token's three digit rows xd[d*C + c].
+template <typename ActT>
+__device__ __forceinline__ void write_x_digits4(const ActT* __restrict__ xr, int i, int Ex,
+                                                int8_t* __restrict__ xd, int C) {
+  const int c = i * 4;
+  float v[4];
+  load4_act(xr + c, v);
+  uint32_t w0 = 0, w1 = 0, w2 = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    int d0, d1, d2;
+    split_digits((int)rintf(ldexpf(v[j], Ex)), d0, d1, d2);
+    w0 |= (uint32_t)(d0 & 0xFF) << (8 * j);
+    w1 |= (uint32_t)(d1 & 0xFF) << (8 * j);
+    w2 |= (uint32_t)(d2 & 0xFF) << (8 * j);
+  }
+  *(uint32_t*)(xd + c) = w0;
+  *(uint32_t*)(xd + C + c) = w1;
+  *(uint32_t*)(xd + 2 * (size_t)C + c) = w2;
+}
+
 template <typename ActT>
 __global__ __launch_bounds__(kBigThreads) void decode_prep_kernel(
     const ActT* __restrict__ x, const ActT* __restrict__ wr, const float* __restrict__ bias,
@@ -456,6 +478,24 @@ __global__ __launch_bounds__(kBigThreads) void decode_prep_kernel(
     }
     __syncthreads();
   }
+  if (T == 1 && E <= 64 && k + S <= 64) {
+    // one token: nothing waits after the logits.  Wave 0 selects and writes
+    // the descriptors from registers; wave 1 makes the same selection (same
+    // keys, same order) for the optional outputs; the other waves write the
+    // digits of x.
+    const int xe = kFixBits - exp_bound(xmax[0]);
+    if (wave == 0) {
+      decode_work_one_token(lg[0], E, k, S, softmax_all, xe, slot_s, ep, work, max_active);
+    } else if (wave == 1) {
+      if (logits_out)
+        for (int e = lane; e < E; e += 64) logits_out[e] = lg[0][e];
+      topk_rank(lg[0], E, k, softmax_all, idx_s, w_s, sel_e[0], sel_v[0]);
+      decode_outputs_small(idx_s, w_s, 1, k, E, S, o, cnt_s);
+    } else {
+      for (int i = tid - 128; i < C / 4; i += kBigThreads - 128) write_x_digits4(x, i, xe, xdig, C);
+    }
+    return;
+  }
   if (wave < T) {
     const int t = wave;
     if (logits_out)
@@ -484,23 +524,8 @@ __global__ __launch_bounds__(kBigThreads) void decode_prep_kernel(
   const int w0d = small ? 2 : 1;
   const int q4 = C / 4, n4 = T * q4;
   for (int i = tid - 64 * w0d; i < n4; i += kBigThreads - 64 * w0d) {
-    const int t = i / q4, c = (i - t * q4) * 4;
-    const int Ex = xe_s[t];
-    float v[4];
-    load4_act(x + (size_t)t * C + c, v);
-    uint32_t w0 = 0, w1 = 0, w2 = 0;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      int d0, d1, d2;
-      split_digits((int)rintf(ldexpf(v[j], Ex)), d0, d1, d2);
-      w0 |= (uint32_t)(d0 & 0xFF) << (8 * j);
-      w1 |= (uint32_t)(d1 & 0xFF) << (8 * j);
-      w2 |= (uint32_t)(d2 & 0xFF) << (8 * j);
-    }
-    int8_t* d0p = xdig + (size_t)t * kDigits * C + c;
-    *(uint32_t*)(d0p) = w0;
-    *(uint32_t*)(d0p + C) = w1;
-    *(uint32_t*)(d0p + 2 * C) = w2;
+    const int t = i / q4;
+    write_x_digits4(x + (size_t)t * C, i - t * q4, xe_s[t], xdig + (size_t)t * kDigits * C, C);
   }
 }
 

@@ -151,6 +151,37 @@ __device__ void logits_ksplit_bf16(const uint16_t* __restrict__ x, const uint16_
 // v_readlane, so the count needs no memory round trips.  The combine weights
 // are a softmax in fp32, summed in selection order.  sel_e/sel_v: this wave's
 // LDS scratch.
+// The selection of topk_rank with E <= 64 experts, one per lane: lane e
+// learns whether it is selected, its position and its combine weight.
+__device__ __forceinline__ void topk_lane64(const float* lgrow, int E, int k, int softmax_all,
+                                            bool& sel, int& rank, float& w) {
+  const int lane = threadIdx.x & 63;
+  const bool in = lane < E;
+  const float v = in ? lgrow[lane] : 0.f;
+  const uint32_t key = f32_order_key(v);
+  rank = 0;
+#pragma unroll 1
+  for (int l2 = 0; l2 < E; ++l2) {
+    const uint32_t k2 = (uint32_t)__builtin_amdgcn_readlane((int)key, l2);
+    rank += (k2 > key) || (k2 == key && l2 < lane);
+  }
+  sel = in && rank < k;
+  const int l0 = __builtin_ctzll(__ballot(sel && rank == 0));
+  const float vmax = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l0));
+  const float ex = in ? expf(v - vmax) : 0.f;
+  float denom = 0.f;
+  if (softmax_all) {
+    denom = wave_sum(ex);
+  } else {
+#pragma unroll 1
+    for (int j = 0; j < k; ++j) {
+      const int lj = __builtin_ctzll(__ballot(sel && rank == j));
+      denom += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ex), lj));
+    }
+  }
+  w = ex / denom;
+}
+
 __device__ __forceinline__ void topk_rank(const float* lgrow, int E, int k, int softmax_all,
                                           int32_t* idx_a, float* w_a, int* sel_e, float* sel_v) {
   constexpr int kPer = MIRA_MAX_EXPERTS / 64;  // experts per lane
@@ -158,32 +189,13 @@ __device__ __forceinline__ void topk_rank(const float* lgrow, int E, int k, int 
   if (E <= 64) {
     // one expert per lane: the selection stays in registers (the same keys,
     // exponentials and sum order as below, so the results are identical)
-    const bool in = lane < E;
-    const float v = in ? lgrow[lane] : 0.f;
-    const uint32_t key = f32_order_key(v);
-    int rank = 0;
-#pragma unroll 1
-    for (int l2 = 0; l2 < E; ++l2) {
-      const uint32_t k2 = (uint32_t)__builtin_amdgcn_readlane((int)key, l2);
-      rank += (k2 > key) || (k2 == key && l2 < lane);
-    }
-    const bool sel = in && rank < k;
-    const int l0 = __builtin_ctzll(__ballot(sel && rank == 0));
-    const float vmax = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l0));
-    const float ex = in ? expf(v - vmax) : 0.f;
-    float denom = 0.f;
-    if (softmax_all) {
-      denom = wave_sum(ex);
-    } else {
-#pragma unroll 1
-      for (int j = 0; j < k; ++j) {
-        const int lj = __builtin_ctzll(__ballot(sel && rank == j));
-        denom += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ex), lj));
-      }
-    }
+    bool sel;
+    int rank;
+    float w;
+    topk_lane64(lgrow, E, k, softmax_all, sel, rank, w);
     if (sel) {
       idx_a[rank] = lane;
-      w_a[rank] = ex / denom;
+      w_a[rank] = w;
     }
     return;
   }
@@ -509,6 +521,52 @@ __device__ inline void decode_work_small(const int32_t* idx_s, const float* w_s,
   for (int aa = nr + S + lane; aa < max_active; aa += 64) work[aa].group = -1;
   bits = wave_or(bits);
   if (lane == 0 && ep.status) *ep.status = bits;
+}
+
+// DecodeWork descriptors and the residency status of a one-token call with
+// E <= 64 experts and k + S <= 64 groups (one wave), straight from the
+// selection in registers: the selected experts in expert order (group a at
+// position a, one pair each), then the shared experts.  xe: the token's
+// fixed-point exponent.  The same descriptors as decode_work_small.
+__device__ inline void decode_work_one_token(const float* lgrow, int E, int k, int S,
+                                             int softmax_all, int xe, const int* slot_s,
+                                             const ExpertPool& ep, DecodeWork* __restrict__ work,
+                                             int max_active) {
+  const int lane = threadIdx.x & 63;
+  bool sel;
+  int rank;
+  float w;
+  topk_lane64(lgrow, E, k, softmax_all, sel, rank, w);
+  const uint64_t lt = lane ? (~0ull >> (64 - lane)) : 0ull;
+  const int a = __popcll(__ballot(sel) & lt);
+  int bits = 0;
+  if (sel) {
+    const int slot = slot_s[lane];
+    bits = slot < 0 ? 1 : (slot >= ep.n_slots ? 2 : 0);
+    DecodeWork* wk = work + a;
+    wk->group = lane;
+    wk->slot = slot;
+    wk->off = a;
+    wk->n = 1;
+    wk->tok[0] = 0;
+    wk->xe[0] = xe;
+    wk->w[0] = w;
+  }
+  if (lane < S) {
+    const int slot = slot_s[E + lane];
+    bits = slot < 0 ? 1 : (slot >= ep.n_slots ? 2 : 0);
+    DecodeWork* wk = work + k + lane;
+    wk->group = E + lane;
+    wk->slot = slot;
+    wk->off = k + lane;
+    wk->n = 1;
+    wk->tok[0] = 0;
+    wk->xe[0] = xe;
+    wk->w[0] = 1.0f;
+  }
+  for (int aa = k + S + lane; aa < max_active; aa += 64) work[aa].group = -1;
+  const int st = (__ballot(bits & 1) ? 1 : 0) | (__ballot(bits & 2) ? 2 : 0);
+  if (lane == 0 && ep.status) *ep.status = st;
 }
 
 // The caller's optional routing outputs of a call with T*k <= 64 pairs (one
