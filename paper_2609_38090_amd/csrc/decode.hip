@@ -8,7 +8,10 @@
 // int8 operand column, so the products and sums are exact int32 and the only
 // rounding is the fixed-point step and the final fp32 arithmetic.  x has three
 // digits (2^-22 of the token's maximum); H' three (2^-22 of its 64-row block
-// maximum) when the call has at most 5 tokens, else two (2^-14).  Since the
+// maximum) when the call has at most 5 tokens, else two (2^-14).  A one-token
+// call instead gives every 16-row tile of H' its own exponent (three digits):
+// its gate/up splits the tiles evenly over the CUs, and its down kernel gives
+// each (tile, digit) pair of a k-step its own operand column.  Since the
 // shared scale sigma_r factors out (section IV-B), y = Qd H' with
 // H' = sigma (.) silu(G) (.) U.
 #include "decode_dev.h"
@@ -16,9 +19,9 @@
 namespace mira {
 
 // ---------------------------------------------------------------------------
-// Gate/up + SwiGLU.  Workgroup = (non-empty expert a, block of 64 rows of R);
-// the digits of x come from the workspace (xdig[(t*3 + d)*C + c], written by
-// the decode preparation kernel).
+// Gate/up + SwiGLU of calls with several tokens.  Workgroup = (non-empty
+// expert a, block of 64 rows of R); the digits of x come from the workspace
+// (xdig[(t*3 + d)*C + c], written by the decode preparation kernel).
 // ---------------------------------------------------------------------------
 // With XL (INT4, one token group, C <= kXlMaxC) the workgroup first copies
 // the digit rows of its tokens into LDS (row stride C + 16 bytes, so the 16
