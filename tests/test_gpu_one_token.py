@@ -5,8 +5,9 @@ exponent, and the down kernel one operand column per (tile, digit) pair;
 the gate/up kernel hands the slot it resolved to the down kernel.  These
 shapes cover tile counts far below one per CU, a ragged last workgroup, the
 8-wave cap with more workgroups than CUs, one active expert, shared
-experts, fp32 activations, both weight formats, and the INT4 fallback to
-the block kernel above C = 4096.  Bars: routing bit-exact and every output
+experts, more than 64 experts (the general preparation path), fp32
+activations, both weight formats, and the INT4 fallback to the block kernel
+above C = 4096.  Bars: routing bit-exact and every output
 row within the error bars (run_and_check), and the decode floor of one
 token."""
 import numpy as np
@@ -41,6 +42,10 @@ CASES = [
     ("int4_shared", _cfg("one_i4_shared", 608, C=1024, E=8, k=2, R=1536, S=1, zipf_s=1.2), "int4"),
     # C above the LDS staging limit: the INT4 block kernel without staging
     ("int4_wide", _cfg("one_i4_wide", 609, C=4224, E=4, k=2, R=256), "int4"),
+    # more than 64 experts: the general preparation path (two experts per
+    # lane in the top-k) in front of the tile kernels
+    ("many_experts", _cfg("one_e96", 611, C=256, E=96, k=4, R=128, S=1, zipf_s=1.0), "int8"),
+    ("int4_many_experts", _cfg("one_i4_e96", 612, C=256, E=96, k=4, R=128, S=1, zipf_s=1.0), "int4"),
 ]
 
 
