@@ -39,9 +39,14 @@ def test_packed_expert_bytes_closed_form():
     assert mira.mira_packed_expert_bytes(64, -1) == 0
 
 
-def test_workspace_bytes_monotone_and_validated():
-    s = mira.MoEShape(2048, 1408, 64, 6, 2, mira.MIRA_BF16)
-    sizes = [mira.mira_workspace_bytes(s, t) for t in (1, 8, 16, 17, 512, 2048)]
+@pytest.mark.parametrize("shape", [(2048, 1408, 64, 6, 2), (4096, 14336, 8, 2, 0), (64, 8192, 256, 16, 0),
+                                   (256, 4096, 16, 8, 2), (128, 64, 1, 1, 0)])
+def test_workspace_bytes_monotone_and_validated(shape):
+    # a workspace sized for max_tokens must serve every smaller call, also a
+    # one-token call, whose H' exponents are per 16-row tile instead of per
+    # 64-row block
+    s = mira.MoEShape(*shape, mira.MIRA_BF16)
+    sizes = [mira.mira_workspace_bytes(s, t) for t in list(range(1, 40)) + [512, 2048]]
     assert all(a <= b for a, b in zip(sizes, sizes[1:]))
     assert all(v % 256 == 0 for v in sizes)
     with pytest.raises(mira.MiraError):
