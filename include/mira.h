@@ -220,8 +220,9 @@ size_t mira_workspace_bytes(const mira_shape* s, int32_t max_tokens);
  * the experts run on int8 matrix cores with the packed bytes as one operand
  * and the activations as fixed-point digits as the other, so the sums are
  * exact integers and the rounding is that of the fixed points: x at 2^-22 of
- * each token's maximum, H' at 2^-22 of the maximum of its 64-row block when
- * the call has at most 5 tokens and 2^-14 above.  Otherwise (or with
+ * each token's maximum, H' at 2^-22 of the maximum of its 16-row tile for a
+ * one-token call, of its 64-row block for 2 to 5 tokens, and 2^-14 of its
+ * 64-row block above.  Otherwise (or with
  * MIRA_FLAG_FORCE_PREFILL) the int8 weights are widened exactly to bf16 for
  * bf16 matrix cores with fp32 accumulation and H' is held in bf16; with fp32
  * activations x and H' are each carried as a high and a low bf16 part and
