@@ -89,3 +89,18 @@ def test_one_token_missing_selected_expert(mira, fmt):
     ref = oracle.moe_forward(o_x, o_wr, o_b, _Zero(LazyBlobs(lay)), cfg.k, cfg.C, cfg.R, fmt=fmt)["out"]
     assert np.isfinite(res["out"]).all()
     assert_ffn_close(res["out"], ref, f"one token, expert {e0} missing, {fmt}")
+
+
+@pytest.mark.parametrize("fmt", ["int8", "int4"])
+def test_one_token_reads_nothing_stale_from_the_workspace(mira, fmt):
+    """Every tile exponent, digit and resolved slot the down kernel reads is
+    written in the same call: a workspace filled with NaN bytes and one filled
+    with zero bytes give bit-identical outputs.  (A one-token call right
+    after a 16-token call on the same scratch is the no-alloc test's case.)"""
+    cfg = _cfg("one_ws", 613, C=512, E=8, k=2, R=1024, S=1, zipf_s=1.0)
+    lay = Layer(cfg, fmt=fmt)
+    a = lay.run(ws_fill=0xFF)
+    b = lay.run(ws_fill=0x00)
+    for key in ("out", "idx", "w", "counts", "status"):
+        assert np.array_equal(a[key], b[key]), key
+    assert np.isfinite(a["out"]).all()
