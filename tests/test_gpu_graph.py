@@ -1,7 +1,8 @@
 """A layer call captured into a HIP graph (torch.cuda.CUDAGraph): the forward
 path makes no allocation, copy, memset or host synchronisation, so it
 captures; every replay, with eager work and synchronisations between the
-replays, gives the eager result bit for bit (decode, INT4 decode, prefill)."""
+replays, gives the eager result bit for bit (decode, INT4 decode, one-token
+decode in both formats, prefill)."""
 import numpy as np
 import pytest
 import torch
@@ -16,7 +17,8 @@ DEC = MoEConfig("graph_dec", 141, T=16, C=256, E=8, k=2, R=512, zipf_s=1.2)
 PRE = MoEConfig("graph_pre", 142, T=40, C=128, E=64, k=6, R=128, S=2, zipf_s=1.0)
 
 
-@pytest.mark.parametrize("cfg,T,fmt", [(DEC, 3, "int8"), (DEC, 2, "int4"), (PRE, 40, "int8")])
+@pytest.mark.parametrize("cfg,T,fmt", [(DEC, 3, "int8"), (DEC, 2, "int4"), (DEC, 1, "int8"), (DEC, 1, "int4"),
+                                       (PRE, 40, "int8")])
 def test_graph_replays_match_eager(mira, cfg, T, fmt):
     lay = Layer(cfg, T=T, fmt=fmt)
     ref = lay.run()
