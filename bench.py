@@ -54,9 +54,9 @@ PROF_EVERY = 8  # steps timed with events: one layer-copy rotation in every 8
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 TRAFFIC = {
     ("decode_gateup", "mixtral_decode"): dict(sources=("decode.hip", "decode_dev.h", "int4_format.h"),
-                                               sha="ec50a0c39ea6a449", fetch_kib=114834.6, write_kib=110.3),
+                                               sha="2b2b8f93748da802", fetch_kib=114834.8, write_kib=110.3),
     ("decode_gateup", "mixtral_decode_int4"): dict(sources=("decode.hip", "decode_dev.h", "int4_format.h"),
-                                                    sha="ec50a0c39ea6a449", fetch_kib=61053.4, write_kib=110.1),
+                                                    sha="2b2b8f93748da802", fetch_kib=61622.0, write_kib=110.1),
     ("prefill_gateup", "mixtral_prefill"): dict(sources=("prefill.hip",), sha="8d87e7443ab4d714",
                                                  fetch_kib=600413.4, write_kib=38203.4),
     ("prefill_gateup", "fine_grained"): dict(sources=("prefill.hip",), sha="8d87e7443ab4d714",

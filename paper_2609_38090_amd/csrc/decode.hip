@@ -29,6 +29,10 @@ namespace mira {
 // from there.
 constexpr int kXlMaxC = 4096;
 constexpr int kXlUnroll = 16;  // k-steps per weight batch
+// k-steps per weight batch of the one-token INT4 tile kernel (6 KB per wave):
+// a wave holds one tile and cannot issue its next loads while it unpacks and
+// scales a batch, and shorter batches measured faster than 4, 8 or 16 steps
+constexpr int kTileI4Unroll = 6;
 
 template <int NG, bool I4, bool XL>
 __device__ __forceinline__ void decode_gateup_body(int C, int R, const ExpertPool& ep,
@@ -198,8 +202,8 @@ __global__ __launch_bounds__(64 * kTileMaxWaves) void decode_gateup_tile_i4_kern
   const auto load_x = [&](int, int ks) { return bv ? *(const v4i*)(xr + ks * 64) : zero16(); };
   float accg[1][4], accu[1][4];
   const bool bva[1] = {bv};
-  gateup_tile_stream_i4<1, kXlUnroll, true>(C, R, rt, (const uint8_t*)ep.pool + (size_t)slot * ep.stride,
-                                            bva, load_x, accg, accu);
+  gateup_tile_stream_i4<1, kTileI4Unroll, true>(C, R, rt, (const uint8_t*)ep.pool + (size_t)slot * ep.stride,
+                                                bva, load_x, accg, accu);
   // 2^-E of the token's fixed point, and 1/16 for the nibble operand (16*q)
   const bool lead = bv && r16 == 0;
   const float xs = bv ? ldexpf(1.f, -xe - 4) : 0.f;
