@@ -57,6 +57,10 @@ TRAFFIC = {
                                                sha="2b2b8f93748da802", fetch_kib=114834.8, write_kib=110.3),
     ("decode_gateup", "mixtral_decode_int4"): dict(sources=("decode.hip", "decode_dev.h", "int4_format.h"),
                                                     sha="2b2b8f93748da802", fetch_kib=61622.0, write_kib=110.1),
+    # the beam stack's decode_gateup: the mean over all its launches (32
+    # layers, 5.38 selected experts per layer on average)
+    ("decode_gateup", "beam_stack"): dict(sources=("decode.hip", "decode_dev.h", "int4_format.h"),
+                                          sha="2b2b8f93748da802", fetch_kib=308765.0, write_kib=560.3),
     ("prefill_gateup", "mixtral_prefill"): dict(sources=("prefill.hip",), sha="8d87e7443ab4d714",
                                                  fetch_kib=600413.4, write_kib=38203.4),
     ("prefill_gateup", "fine_grained"): dict(sources=("prefill.hip",), sha="8d87e7443ab4d714",
@@ -640,7 +644,8 @@ def stack_roofline(cfg, L, fmt, prof, active):
     achieved = gu_bytes / dur / 1e9
     return {"bound": "hbm", "kernel": "decode_gateup", "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None, "avg_us": round(dur * 1e6, 2), "algorithmic_bytes_per_launch": int(gu_bytes),
+            "traffic": traffic_bytes("decode_gateup", cfg.name if fmt == "int8" else f"{cfg.name}_int4"),
+            "avg_us": round(dur * 1e6, 2), "algorithmic_bytes_per_launch": int(gu_bytes),
             "timed_launches": cnt}
 
 
